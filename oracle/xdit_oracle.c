@@ -1,0 +1,208 @@
+/*
+ * fp64 CPU oracle for the DiT attention hot path of xDiT (arXiv 2411.01738).
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product library calls, links or
+ * includes this file; only the tests, the smoke check and the CPU-baseline leg
+ * of the benchmark load it. It shares no code, header or constant with the HIP
+ * path.
+ *
+ * It writes out the plain definitions the GPU kernels must reproduce, in
+ * double precision, one query row at a time, with no tiling, no online
+ * rescaling and no fusion:
+ *
+ *   attention      full (non-causal) multi-head self-attention softmax(s*Q K^T) V
+ *                  with s = 1/sqrt(d)  (Section 2 "Diffusion Transformers";
+ *                  Section 4.1.2 says DiT attention is full, not causal)
+ *   chunk          the same over one K/V chunk, also returning the natural-log
+ *                  log-sum-exp of the scaled scores (Section 4.1.1: SP-Ring is a
+ *                  parallel FlashAttention over P2P-exchanged K/V sub-blocks)
+ *   merge          recombination of chunk partials (Section 4.1.1: the sharded
+ *                  computation gives the same result as the serial one)
+ *   patch          PipeFusion patch step: the patch's rows of the layer's
+ *                  full-sequence K/V buffer are overwritten with fresh K/V, the
+ *                  rest keep stale K/V from the previous diffusion step, and the
+ *                  patch's queries attend over the whole buffer
+ *                  (Section 4.1.2, PipeFusion; Section 4.1.4 on storing
+ *                  communicated K/V into that buffer)
+ *
+ * Layout (a reading: the paper does not fix one): activations are
+ * sequence-major [B, N, H, d] with d contiguous; the K/V buffer is
+ * [2, B, N, H, d] (plane 0 = K, plane 1 = V); LSE is [B, H, Nq].
+ * Inputs are float arrays holding the values exactly as uploaded to the GPU
+ * (bf16 values are exact in float); every product and sum is taken in double.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define IDX4(b, n, h, c, N, H, D) ((((int64_t)(b) * (N) + (n)) * (H) + (h)) * (D) + (c))
+
+int xo_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void xo_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/*
+ * One output row of attention, by definition:
+ *   s_j   = scale * sum_c q_c k_jc
+ *   m     = max_j s_j
+ *   lse   = m + ln sum_j exp(s_j - m)
+ *   o_c   = sum_j exp(s_j - lse) v_jc
+ * With no keys, o = 0 and lse = -inf.  `s` is caller scratch of nk doubles.
+ */
+static void attention_row(const float* q, const float* k, const float* v,
+                          int64_t nk, int64_t row_stride, int64_t d, double scale,
+                          double* s, double* o, double* lse) {
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    if (nk == 0) {
+        *lse = -INFINITY;
+        return;
+    }
+    double m = -INFINITY;
+    for (int64_t j = 0; j < nk; ++j) {
+        const float* kj = k + j * row_stride;
+        double dot = 0.0;
+        for (int64_t c = 0; c < d; ++c) dot += (double)q[c] * (double)kj[c];
+        s[j] = scale * dot;
+        if (s[j] > m) m = s[j];
+    }
+    double l = 0.0;
+    for (int64_t j = 0; j < nk; ++j) l += exp(s[j] - m);
+    const double L = m + log(l);
+    for (int64_t j = 0; j < nk; ++j) {
+        const double p = exp(s[j] - L);
+        const float* vj = v + j * row_stride;
+        for (int64_t c = 0; c < d; ++c) o[c] += p * (double)vj[c];
+    }
+    *lse = L;
+}
+
+/*
+ * Attention of the queries q [B, Nq, H, d] over keys k and values v
+ * [B, Nk, H, d], scale 1/sqrt(d).
+ *
+ * rows: indices of the query rows to evaluate (NULL = all Nq rows in order);
+ *       nrows: how many.  out is [B, nrows, H, d] and lse is [B, H, nrows],
+ *       both double; lse may be NULL.
+ * Returns 0, or -1 on a bad argument.
+ */
+int xo_attention(const float* q, const float* k, const float* v,
+                 int64_t B, int64_t Nq, int64_t Nk, int64_t H, int64_t d,
+                 const int64_t* rows, int64_t nrows, double* out, double* lse) {
+    if (B < 0 || Nq < 0 || Nk < 0 || H < 0 || d <= 0 || nrows < 0) return -1;
+    if (rows == NULL && nrows != Nq) return -1;
+    for (int64_t r = 0; rows != NULL && r < nrows; ++r)
+        if (rows[r] < 0 || rows[r] >= Nq) return -1;
+    const double scale = 1.0 / sqrt((double)d);
+    const int64_t total = B * H * nrows;
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)(Nk > 0 ? Nk : 1));
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t t = 0; t < total; ++t) {
+            const int64_t r = t % nrows;
+            const int64_t h = (t / nrows) % H;
+            const int64_t b = t / (nrows * H);
+            const int64_t i = rows ? rows[r] : r;
+            double row_lse;
+            attention_row(q + IDX4(b, i, h, 0, Nq, H, d), k + IDX4(b, 0, h, 0, Nk, H, d),
+                          v + IDX4(b, 0, h, 0, Nk, H, d), Nk, H * d, d, scale, s,
+                          out + IDX4(b, r, h, 0, nrows, H, d), &row_lse);
+            if (lse) lse[(b * H + h) * nrows + r] = row_lse;
+        }
+        free(s);
+    }
+    return 0;
+}
+
+/*
+ * Merge of n attention partials (o_r [B, Nq, H, d], lse_r [B, H, Nq]), each
+ * computed over one K/V chunk, into attention over the union of the chunks:
+ *   M = max_r lse_r,  L = M + ln sum_r exp(lse_r - M),
+ *   o = sum_r exp(lse_r - L) o_r.
+ * A partial with lse_r = -inf (an empty chunk) has weight 0; if every partial
+ * is empty, o = 0 and L = -inf.
+ * outs/lses: arrays of n pointers (float values as stored by the producer).
+ * out [B, Nq, H, d] and lse_out [B, H, Nq] (may be NULL) are double.
+ */
+int xo_merge(const float* const* outs, const float* const* lses, int32_t n,
+             int64_t B, int64_t Nq, int64_t H, int64_t d, double* out, double* lse_out) {
+    if (n < 1 || B < 0 || Nq < 0 || H < 0 || d <= 0) return -1;
+    const int64_t total = B * H * Nq;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < total; ++t) {
+        const int64_t i = t % Nq;
+        const int64_t h = (t / Nq) % H;
+        const int64_t b = t / (Nq * H);
+        const int64_t lidx = (b * H + h) * Nq + i;
+        double M = -INFINITY;
+        for (int32_t r = 0; r < n; ++r)
+            if ((double)lses[r][lidx] > M) M = (double)lses[r][lidx];
+        double* o = out + IDX4(b, i, h, 0, Nq, H, d);
+        for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+        if (M == -INFINITY) {
+            if (lse_out) lse_out[lidx] = -INFINITY;
+            continue;
+        }
+        double sum = 0.0;
+        for (int32_t r = 0; r < n; ++r) sum += exp((double)lses[r][lidx] - M);
+        const double L = M + log(sum);
+        for (int32_t r = 0; r < n; ++r) {
+            const double w = exp((double)lses[r][lidx] - L);
+            const float* orow = outs[r] + IDX4(b, i, h, 0, Nq, H, d);
+            for (int64_t c = 0; c < d; ++c) o[c] += w * (double)orow[c];
+        }
+        if (lse_out) lse_out[lidx] = L;
+    }
+    return 0;
+}
+
+/*
+ * PipeFusion patch step, update half: rows [off, off+len) of both planes of
+ * kv_buf [2, B, N, H, d] are replaced by fresh_k / fresh_v [B, len, H, d];
+ * every other row keeps its (stale) value.  Exact copy.
+ */
+int xo_patch_update(float* kv_buf, int64_t off, int64_t len, const float* fresh_k,
+                    const float* fresh_v, int64_t B, int64_t N, int64_t H, int64_t d) {
+    if (off < 0 || len < 0 || off + len > N || B < 0 || H < 0 || d <= 0) return -1;
+    const int64_t plane = B * N * H * d;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t i = 0; i < len; ++i)
+            for (int64_t h = 0; h < H; ++h)
+                for (int64_t c = 0; c < d; ++c) {
+                    kv_buf[IDX4(b, off + i, h, c, N, H, d)] = fresh_k[IDX4(b, i, h, c, len, H, d)];
+                    kv_buf[plane + IDX4(b, off + i, h, c, N, H, d)] =
+                        fresh_v[IDX4(b, i, h, c, len, H, d)];
+                }
+    return 0;
+}
+
+/*
+ * PipeFusion patch step: update kv_buf in place (above), then the patch's
+ * queries q [B, len, H, d] attend over the whole updated buffer, so the fresh
+ * slice is visible to this step's own attention.  rows/nrows/out/lse as in
+ * xo_attention (rows index the patch's queries).
+ */
+int xo_patch(const float* q, float* kv_buf, int64_t off, int64_t len, const float* fresh_k,
+             const float* fresh_v, int64_t B, int64_t N, int64_t H, int64_t d,
+             const int64_t* rows, int64_t nrows, double* out, double* lse) {
+    int rc = xo_patch_update(kv_buf, off, len, fresh_k, fresh_v, B, N, H, d);
+    if (rc) return rc;
+    return xo_attention(q, kv_buf, kv_buf + B * N * H * d, B, len, N, H, d, rows, nrows, out,
+                        lse);
+}
