@@ -1,0 +1,255 @@
+"""Benchmark of the DiT attention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload pixart]
+
+One step = one pass of the whole hot path for one layer on the chosen
+workload (default: Pixart 1024px, B=2 H=16 d=72, 4096 tokens):
+  * the M PipeFusion patch steps in order (each call writes its fresh K/V
+    slice into the layer's buffer and attends over the fresh/stale buffer),
+  * the sequence-parallel share: chunk attention of the local query shard over
+    each K/V chunk (O and LSE), then the LSE merge of the partials.
+Inputs are synthetic (seeded N(0,1); stale K/V = fresh + N(0, 0.05^2)) and
+resident in HBM before timing starts.  W untimed steps, then K timed steps
+between synchronisations; HIP events around every call give each kernel's
+average duration.  Prints ONE JSON line.
+
+`value` is algorithmic attention FLOP/s (4*B*H*Nq*Nk*d per call) over the
+whole step.  `roofline` refers to the kernel with the largest share of the
+step's time.  `cpu_baseline` times the fp64 oracle on a bounded row sample of
+the same workload on the host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector peak (published)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
+
+# HBM traffic per launch of the dominant kernel, from rocprofv3 --pmc
+# FETCH_SIZE / WRITE_SIZE, scaled by the copy-kernel calibration factor.
+# None until counters for the current kernel build are taken.
+MEASURED_TRAFFIC = {}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="pixart",
+                    choices=["tiny", "pixart", "sd3", "flux", "cog"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample (0 = skip)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, t, target_s: float):
+    """fp64 oracle on a bounded sample of the workload: whole calls of the step
+    in order (patch steps, else chunk steps) until about target_s seconds have
+    been spent; when one call alone would take far longer, an evenly spaced
+    subset of its query rows.  Scaled to TFLOP/s of algorithmic work."""
+    import numpy as np
+
+    import oracle
+
+    orc = oracle.get()
+    jobs = []  # (description, nq_total, nk, run(rows))
+    if w.patches():
+        kv = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
+        for p, (off, ln) in enumerate(w.patches()):
+            q = t.q[:, off:off + ln].copy()
+            fk = t.k_fresh[:, off:off + ln].copy()
+            fv = t.v_fresh[:, off:off + ln].copy()
+            jobs.append((f"patch step {p}", ln, w.N,
+                         lambda rows, q=q, off=off, fk=fk, fv=fv: orc.patch(q, kv, off, fk, fv,
+                                                                           rows=rows)))
+    else:
+        q0, q1 = w.sp_q
+        q = t.q[:, q0:q1].copy()
+        for r, (s, e) in enumerate(w.sp_chunks):
+            k = t.k_fresh[:, s:e].copy()
+            v = t.v_fresh[:, s:e].copy()
+            jobs.append((f"chunk {r}", q1 - q0, e - s,
+                         lambda rows, k=k, v=v: orc.attention(q, k, v, rows=rows)))
+
+    # calibrate on a few rows of the first call
+    desc0, nq0, nk0, run0 = jobs[0]
+    probe = np.linspace(0, nq0 - 1, min(64, nq0)).astype(np.int64)
+    t0 = time.perf_counter()
+    run0(probe)
+    per_row = (time.perf_counter() - t0) / len(probe)
+    flops, spent, parts = 0.0, 0.0, []
+    for desc, nq, nk, run in jobs:
+        left = target_s - spent
+        if left <= 0.2 * target_s and parts:
+            break
+        n = nq if per_row * nq <= left else max(1, int(left / per_row))
+        rows = np.arange(nq, dtype=np.int64) if n >= nq else np.linspace(0, nq - 1, n).astype(np.int64)
+        t0 = time.perf_counter()
+        run(rows)
+        spent += time.perf_counter() - t0
+        flops += w.attn_flops(len(rows), nk)
+        parts.append(f"{desc} ({len(rows)}/{nq} rows)")
+    return {
+        "value": flops / spent / 1e12,
+        "unit": "TFLOP/s",
+        "cores": orc.num_threads(),
+        "kind": "oracle",
+        "sample": "; ".join(parts) + f"; all {w.B * w.H} (batch, head) pairs, fp64,"
+                  f" {spent:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2411_01738_amd import _lib
+    from paper_2411_01738_amd.hotpath import HotPath
+    from paper_2411_01738_amd.inputs import WORKLOADS, generate
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    _lib.lib()  # fails loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    t = generate(w)
+    hp = HotPath(w, t)
+    stream = torch.cuda.current_stream()
+
+    # each entry: (kind, callable, flops, bytes)
+    calls = []
+    for p in range(len(hp.patch_q)):
+        calls.append(("patch_attn", lambda p=p: hp.patch_step(p), hp.patch_flops(p), 0.0))
+    if hp.sp_q is not None:
+        for r in range(len(hp.chunk_k)):
+            calls.append(("chunk_attn", lambda r=r: hp.chunk_step(r), hp.chunk_flops(r), 0.0))
+        calls.append(("lse_merge", hp.merge, 0.0, hp.merge_bytes()))
+
+    for _ in range(args.warmup):
+        hp.step()
+    torch.cuda.synchronize()
+
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in calls] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(args.steps):
+        for i, (_, fn, _, _) in enumerate(calls):
+            ev[s][i][0].record(stream)
+            fn()
+            ev[s][i][1].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+
+    kinds = {}
+    for i, (kind, _, flops, nbytes) in enumerate(calls):
+        d = kinds.setdefault(kind, {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        for s in range(args.steps):
+            d["ms"] += ev[s][i][0].elapsed_time(ev[s][i][1])
+        d["launches"] += args.steps
+        d["flops"] += flops * args.steps
+        d["bytes"] += nbytes * args.steps
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    kern = {}
+    for kind, d in kinds.items():
+        avg_us = d["ms"] * 1e3 / d["launches"]
+        e = {"launches_per_step": d["launches"] // args.steps, "avg_us": round(avg_us, 3)}
+        if d["flops"]:
+            tf = d["flops"] / (d["ms"] / 1e3) / 1e12
+            e.update(tflops=round(tf, 2), frac_peak=round(tf / peak, 4))
+        if d["bytes"]:
+            gbs = d["bytes"] / (d["ms"] / 1e3) / 1e9
+            e.update(gbs=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 4))
+        kern[kind] = e
+
+    # stand-alone K/V-slice update (the patch kernel does it fused): its GB/s
+    if w.patches():
+        from paper_2411_01738_amd import xdit_kv_update
+
+        reps = 20
+        off, ln = w.patches()[0]
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        xdit_kv_update(hp.kv_buf, off, ln, hp.patch_k[0], hp.patch_v[0])
+        a.record(stream)
+        for _ in range(reps):
+            xdit_kv_update(hp.kv_buf, off, ln, hp.patch_k[0], hp.patch_v[0])
+        b.record(stream)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / reps
+        gbs = hp.update_bytes(0) / (us / 1e6) / 1e9
+        kern["kv_update"] = {"avg_us": round(us, 3), "gbs": round(gbs, 1),
+                             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "note": "warm, outside the step"}
+
+    step_flops = hp.step_flops()
+    value = step_flops / (ms_per_step / 1e3) / 1e12
+
+    dom = max(kinds, key=lambda k: kinds[k]["ms"])
+    dd = kinds[dom]
+    avg_s = dd["ms"] / 1e3 / dd["launches"]
+    if dd["flops"]:
+        per_launch = dd["flops"] / dd["launches"]
+        achieved = per_launch / avg_s / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    else:
+        per_launch = dd["bytes"] / dd["launches"]
+        achieved = per_launch / avg_s / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = MEASURED_TRAFFIC.get((w.name, dom))
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(w, t, args.cpu_seconds)
+
+    desc = {"tiny": "tiny fp32: B=1 H=2 d=64, 256 tokens, M=4 patch steps + 4-chunk SP share",
+            "pixart": "pixart-1024px: B=2 H=16 d=72, 4096 tokens, M=4 patch steps"
+                      " + 4-chunk SP share (Q 1024 rows)",
+            "sd3": "sd3-1024px joint attention: B=2 H=24 d=64, 4096 image + 333 text tokens,"
+                   " M=8 patch steps",
+            "flux": "flux-2048px SP share: B=1 H=24 d=128, Q 4224 rows x 4 chunks of 4224 + merge",
+            "cog": "cogvideox video: B=1 H=48 d=64, 17550 video + 226 text tokens, M=16 patch"
+                   " steps + 8-chunk split (Q all rows) + merge"}[w.name]
+    line = {
+        "metric": "attention TFLOP/s (bf16) per patch/chunk step; merge GB/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": desc, "B": w.B, "H": w.H, "d": w.d, "tokens": w.N,
+                   "patches": len(w.patches()), "sp_chunks": len(w.sp_chunks),
+                   "flops_per_step": step_flops},
+        "kernels": kern,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,153 @@
+/*
+ * xdit.h -- C ABI of the MI355X (gfx950) DiT attention hot path of xDiT
+ * (arXiv 2411.01738): the PipeFusion patch step, the sequence-parallel chunk
+ * step and the log-sum-exp merge of chunk partials, as one GPU executes them.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers: every tensor pointer is a DEVICE pointer, owned by the caller, at
+ *   least 16-byte aligned, to dense row-major storage.  The library allocates
+ *   nothing and keeps no state except a per-thread stream and error message.
+ *   The one exception is xdit_lse_merge's `outs` / `lses`, which are HOST
+ *   arrays holding `n` device pointers.
+ * Layouts (the paper fixes none; this is the layout a QKV projection emits):
+ *   activations  [B, N, H, d]  sequence-major, d contiguous (q, k, v, out,
+ *                              fresh_k, fresh_v, merge partials)
+ *   K/V buffer   [2, B, N, H, d]  plane 0 = K, plane 1 = V
+ *   LSE          [B, H, Nq]    float32, natural log of sum_j exp(s_j) where
+ *                              s_j = (q . k_j) / sqrt(d)
+ * dtype: XDIT_BF16 or XDIT_F32, the element type of every activation tensor
+ *   of a call (LSE is always float32).  bf16 calls compute QK^T and PV on the
+ *   matrix cores with float32 accumulation and round the output to nearest
+ *   even; f32 calls use float32 products throughout.
+ * head_dim: 64, 72 or 128.
+ * Softmax scale: always 1/sqrt(head_dim).  Attention is full (no mask).
+ * Streams: every call is asynchronous on the stream set by xdit_set_stream
+ *   for the calling thread (NULL = the default stream).  Device faults surface
+ *   at the caller's next synchronisation.
+ * Errors: 0 on success, a negative xdit_status otherwise.  Every argument is
+ *   checked before anything is launched, so a rejected call has no side
+ *   effects (the K/V buffer is untouched); xdit_last_error() then describes
+ *   the problem.  NaN / Inf inputs are not checked and propagate.
+ * A pointer may be NULL only where the tensor it stands for has no elements.
+ */
+#ifndef XDIT_H
+#define XDIT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { XDIT_BF16 = 0, XDIT_F32 = 1 };
+
+/* Upper bound on the number of partials one xdit_lse_merge call accepts. */
+#define XDIT_MAX_PARTIALS 64
+
+typedef enum {
+    XDIT_OK = 0,
+    XDIT_ERR_NULL = -1,        /* a required pointer is NULL                  */
+    XDIT_ERR_DTYPE = -2,       /* unknown dtype                               */
+    XDIT_ERR_SHAPE = -3,       /* negative or oversized dimension             */
+    XDIT_ERR_RANGE = -4,       /* patch slice outside the buffer; bad n       */
+    XDIT_ERR_LAYOUT = -5,      /* pointer not 16-byte aligned                 */
+    XDIT_ERR_ALIAS = -6,       /* an output overlaps an input it must not     */
+    XDIT_ERR_UNSUPPORTED = -7, /* head_dim not in {64, 72, 128}               */
+    XDIT_ERR_HIP = -8          /* the HIP runtime refused a launch            */
+} xdit_status;
+
+/*
+ * PipeFusion patch step (Section 4.1.2; buffer contents per Section 4.1.4).
+ *
+ * One layer's full-sequence K/V buffer holds, for every row, either fresh K/V
+ * of the current diffusion step or stale K/V left by the previous step.  The
+ * patch step first overwrites rows [patch_off, patch_off + patch_len) of both
+ * planes with this patch's fresh K/V, then computes attention of the patch's
+ * queries over all seq_len rows of the updated buffer, so the fresh slice is
+ * seen by this call's own attention and by every later call.  Within one
+ * diffusion step, calling this for patches 0..M-1 in order leaves patches
+ * <= p fresh when patch p runs.
+ *
+ *   q        [B, patch_len, H, d]   queries of the patch's rows
+ *   kv_buf   [2, B, seq_len, H, d]  the layer's K/V buffer; MUTATED in place:
+ *                                   afterwards rows [off, off+len) equal
+ *                                   fresh_k / fresh_v bit for bit and every
+ *                                   other row is unchanged
+ *   fresh_k, fresh_v [B, patch_len, H, d]
+ *   out      [B, patch_len, H, d]   attention output
+ * Requires 0 <= patch_off, 0 <= patch_len, patch_off + patch_len <= seq_len.
+ * patch_len = 0 is a no-op.  out must not overlap any input; fresh_k/fresh_v
+ * must not overlap kv_buf.
+ */
+int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patch_len,
+                    const void* fresh_k, const void* fresh_v, void* out,
+                    int64_t batch, int64_t seq_len, int64_t heads, int64_t head_dim,
+                    int32_t dtype);
+
+/*
+ * Sequence-parallel chunk step (Section 4.1.1: SP-Ring computes attention as
+ * a parallel FlashAttention over K/V sub-blocks exchanged peer to peer).
+ * Attention of q over one K/V chunk, returning the normalised partial output
+ * and its log-sum-exp, which xdit_lse_merge combines across chunks.  With the
+ * whole sequence as the chunk this is plain full attention.
+ *
+ *   q    [B, q_len, H, d]
+ *   k, v [B, kv_len, H, d]
+ *   out  [B, q_len, H, d]
+ *   lse  [B, H, q_len] float32, or NULL to skip it
+ * kv_len = 0 gives out = 0 and lse = -inf.  q_len = 0 is a no-op.
+ * out and lse must not overlap q, k or v (or each other).
+ */
+int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, float* lse,
+                    int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                    int64_t head_dim, int32_t dtype);
+
+/*
+ * Log-sum-exp merge of n chunk partials into attention over the union of the
+ * chunks (Section 4.1.1: the sharded computation gives the serial result):
+ *   M = max_r lse_r,  L = M + ln sum_r exp(lse_r - M),
+ *   out = sum_r exp(lse_r - L) * outs[r]      (float32 arithmetic)
+ * A partial with lse = -inf (an empty chunk) has weight 0; if all are -inf,
+ * out = 0 and L = -inf.
+ *
+ *   outs    HOST array of n device pointers, each [B, q_len, H, d] (dtype)
+ *   lses    HOST array of n device pointers, each [B, H, q_len] float32
+ *   n       1 <= n <= XDIT_MAX_PARTIALS
+ *   out     [B, q_len, H, d]; may be exactly outs[r] (in-place), must not
+ *           otherwise overlap a partial
+ *   lse_out [B, H, q_len] float32 merged L, or NULL; must not overlap lses
+ */
+int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n, void* out,
+                   float* lse_out, int64_t batch, int64_t q_len, int64_t heads,
+                   int64_t head_dim, int32_t dtype);
+
+/*
+ * The update half of the patch step on its own (Section 4.1.2): copy the
+ * fresh K/V rows into rows [patch_off, patch_off + patch_len) of kv_buf,
+ * bit for bit, leaving every other row unchanged.  xdit_patch_attn performs
+ * the same update itself; this entry point serves callers that fill the
+ * buffer without attending (e.g. storing K/V received by SP, Section 4.1.4).
+ * Arguments and requirements as for xdit_patch_attn.
+ */
+int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const void* fresh_k,
+                   const void* fresh_v, int64_t batch, int64_t seq_len, int64_t heads,
+                   int64_t head_dim, int32_t dtype);
+
+/* Stream for the calling thread's later launches (a hipStream_t; NULL = the
+ * default stream).  Always returns XDIT_OK. */
+int xdit_set_stream(void* stream);
+void* xdit_get_stream(void);
+
+/* Message describing the calling thread's most recent failure ("" if none).
+ * Valid until that thread's next call into the library. */
+const char* xdit_last_error(void);
+
+/* Library version string. */
+const char* xdit_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XDIT_H */

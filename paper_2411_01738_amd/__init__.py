@@ -1,0 +1,147 @@
+"""MI355X (gfx950) DiT attention hot path of xDiT (arXiv 2411.01738).
+
+Thin binding over the C ABI of libxdit.so (include/xdit.h): each function
+takes torch tensors that already live on the GPU, checks that they are dense,
+reads their sizes, passes raw device pointers and torch's current stream, and
+raises XditError when the library rejects the call.  All arithmetic runs in
+the library's HIP kernels; there is no host or PyTorch fallback.
+
+Layouts: activations [B, N, H, d]; K/V buffer [2, B, N, H, d]; LSE [B, H, Nq]
+float32.  dtypes: bfloat16 or float32 (LSE always float32).
+"""
+from __future__ import annotations
+
+import ctypes
+
+from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XditError, check, lib)
+
+__all__ = ["xdit_patch_attn", "xdit_chunk_attn", "xdit_lse_merge", "xdit_kv_update",
+           "set_stream", "XditError", "XDIT_MAX_PARTIALS", "version"]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return XDIT_BF16
+    if t.dtype == torch.float32:
+        return XDIT_F32
+    raise XditError(-2, f"unsupported dtype {t.dtype}")
+
+
+def _dense(t, name: str, ndim: int):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise XditError(-1, f"{name} must be a GPU tensor")
+    if t.dim() != ndim:
+        raise XditError(-3, f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise XditError(-5, f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _use_current_stream() -> None:
+    lib().xdit_set_stream(_torch().cuda.current_stream().cuda_stream)
+
+
+def set_stream(stream) -> None:
+    """Route later calls of this thread to `stream` (a torch.cuda.Stream or a raw
+    hipStream_t handle).  The functions below always use torch's current stream."""
+    handle = getattr(stream, "cuda_stream", stream)
+    check(lib().xdit_set_stream(handle))
+
+
+def version() -> str:
+    return lib().xdit_version().decode()
+
+
+def xdit_patch_attn(q, kv_buf, patch_off: int, patch_len: int, fresh_k, fresh_v, out) -> None:
+    """PipeFusion patch step: write fresh_k/fresh_v into rows
+    [patch_off, patch_off+patch_len) of kv_buf [2,B,N,H,d] (in place), then
+    out = attention(q, updated K, updated V) for the patch's queries
+    q [B,patch_len,H,d]."""
+    _dense(kv_buf, "kv_buf", 5)
+    for t, n in ((q, "q"), (fresh_k, "fresh_k"), (fresh_v, "fresh_v"), (out, "out")):
+        _dense(t, n, 4)
+    _, B, N, H, d = kv_buf.shape
+    for t, n in ((q, "q"), (fresh_k, "fresh_k"), (fresh_v, "fresh_v"), (out, "out")):
+        if tuple(t.shape) != (B, patch_len, H, d):
+            raise XditError(-3, f"{n} has shape {tuple(t.shape)}, expected {(B, patch_len, H, d)}")
+        if t.dtype != kv_buf.dtype:
+            raise XditError(-2, f"{n} dtype {t.dtype} differs from kv_buf's {kv_buf.dtype}")
+    _use_current_stream()
+    check(lib().xdit_patch_attn(_ptr(q), _ptr(kv_buf), int(patch_off), int(patch_len),
+                                _ptr(fresh_k), _ptr(fresh_v), _ptr(out), B, N, H, d,
+                                _dtype_code(kv_buf)))
+
+
+def xdit_chunk_attn(q, k, v, out, lse=None) -> None:
+    """Chunk attention: out = attention(q, k, v) and, if given,
+    lse [B,H,Nq] = log-sum-exp of the scaled scores (natural log)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out")):
+        _dense(t, n, 4)
+    _dense(lse, "lse", 3)
+    B, Nq, H, d = q.shape
+    Nk = k.shape[1]
+    if tuple(k.shape) != (B, Nk, H, d) or tuple(v.shape) != (B, Nk, H, d):
+        raise XditError(-3, f"k/v shapes {tuple(k.shape)}/{tuple(v.shape)} do not match q")
+    if tuple(out.shape) != (B, Nq, H, d):
+        raise XditError(-3, "out shape differs from q")
+    for t, n in ((k, "k"), (v, "v"), (out, "out")):
+        if t.dtype != q.dtype:
+            raise XditError(-2, f"{n} dtype differs from q's")
+    if lse is not None:
+        torch = _torch()
+        if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, Nq):
+            raise XditError(-3, f"lse must be float32 [B,H,Nq] = {(B, H, Nq)}")
+    _use_current_stream()
+    check(lib().xdit_chunk_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Nq, Nk, H, d,
+                                _dtype_code(q)))
+
+
+def xdit_lse_merge(outs, lses, n: int, out, lse_out=None) -> None:
+    """Merge n chunk partials (outs[r] [B,Nq,H,d], lses[r] [B,H,Nq] float32)
+    into out, and the merged log-sum-exp into lse_out if given."""
+    n = int(n)
+    if n < 1 or n > len(outs) or n > len(lses):
+        raise XditError(-4, f"n = {n} does not match {len(outs)} outs / {len(lses)} lses")
+    _dense(out, "out", 4)
+    _dense(lse_out, "lse_out", 3)
+    B, Nq, H, d = out.shape
+    torch = _torch()
+    for r in range(n):
+        _dense(outs[r], f"outs[{r}]", 4)
+        _dense(lses[r], f"lses[{r}]", 3)
+        if tuple(outs[r].shape) != (B, Nq, H, d) or outs[r].dtype != out.dtype:
+            raise XditError(-3, f"outs[{r}] does not match out")
+        if tuple(lses[r].shape) != (B, H, Nq) or lses[r].dtype != torch.float32:
+            raise XditError(-3, f"lses[{r}] must be float32 {(B, H, Nq)}")
+    optrs = (ctypes.c_void_p * n)(*[outs[r].data_ptr() for r in range(n)])
+    lptrs = (ctypes.c_void_p * n)(*[lses[r].data_ptr() for r in range(n)])
+    _use_current_stream()
+    check(lib().xdit_lse_merge(optrs, lptrs, n, _ptr(out), _ptr(lse_out), B, Nq, H, d,
+                               _dtype_code(out)))
+
+
+def xdit_kv_update(kv_buf, patch_off: int, patch_len: int, fresh_k, fresh_v) -> None:
+    """Copy fresh K/V [B,patch_len,H,d] into rows [patch_off, patch_off+patch_len)
+    of kv_buf [2,B,N,H,d], bit for bit."""
+    _dense(kv_buf, "kv_buf", 5)
+    _dense(fresh_k, "fresh_k", 4)
+    _dense(fresh_v, "fresh_v", 4)
+    _, B, N, H, d = kv_buf.shape
+    for t, nm in ((fresh_k, "fresh_k"), (fresh_v, "fresh_v")):
+        if tuple(t.shape) != (B, patch_len, H, d) or t.dtype != kv_buf.dtype:
+            raise XditError(-3, f"{nm} must be {(B, patch_len, H, d)} of kv_buf's dtype")
+    _use_current_stream()
+    check(lib().xdit_kv_update(_ptr(kv_buf), int(patch_off), int(patch_len), _ptr(fresh_k),
+                               _ptr(fresh_v), B, N, H, d, _dtype_code(kv_buf)))

@@ -1,0 +1,161 @@
+// HBM-bound kernels of the hot path:
+//   * the log-sum-exp merge of chunk partials (Section 4.1.1: SP-Ring's
+//     per-chunk partial attentions recombine into the serial result), and
+//   * the stand-alone K/V-slice update of the PipeFusion buffer
+//     (Section 4.1.2; Section 4.1.4 stores communicated K/V the same way).
+// Both move 16 bytes per lane per access, consecutive lanes on consecutive
+// addresses.
+#include "kernels.h"
+
+#include <math.h>
+
+namespace xdit {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+
+struct MergeArgs {
+    const void* outs[kMaxPartials];
+    const float* lses[kMaxPartials];
+    void* out;
+    float* lse_out;
+    int n, Nq, H, chunks;  // chunks = 16-byte chunks per (b, i, h) row
+    int64_t total;         // B * Nq * H * chunks
+};
+
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+    return (uint32_t)__builtin_bit_cast(uint16_t, a) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// One lane merges one 16-byte chunk of one output row: 8 bf16 or 4 float
+// elements.  Weights w_r = exp(lse_r - M) / sum_r' exp(lse_r' - M), which
+// equals exp(lse_r - L) with L the merged log-sum-exp.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
+    const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (g >= a.total) return;
+    const int cc = (int)(g % a.chunks);
+    const int64_t row = g / a.chunks;  // (b * Nq + i) * H + h
+    const int h = (int)(row % a.H);
+    const int64_t bi = row / a.H;
+    const int i = (int)(bi % a.Nq);
+    const int64_t b = bi / a.Nq;
+    const int64_t lidx = (b * a.H + h) * a.Nq + i;
+    constexpr float kLog2e = 1.4426950408889634f;
+
+    float M = -INFINITY;
+    for (int r = 0; r < a.n; ++r) M = fmaxf(M, a.lses[r][lidx]);
+
+    constexpr int EPC = BF16 ? 8 : 4;
+    float acc[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+    float L = -INFINITY;
+    if (M != -INFINITY) {
+        // (lse_r - M) is exactly 0 for the largest partial, so its weight is
+        // exactly 1 before normalisation and n = 1 reproduces the partial.
+        float sum = 0.f;
+        for (int r = 0; r < a.n; ++r) sum += exp2f((a.lses[r][lidx] - M) * kLog2e);
+        const float inv = 1.f / sum;
+        L = M + logf(sum);
+        const int64_t off = row * a.chunks + cc;  // in 16-byte units
+        for (int r = 0; r < a.n; ++r) {
+            const float w = exp2f((a.lses[r][lidx] - M) * kLog2e) * inv;
+            const u32x4 x = ((const u32x4*)a.outs[r])[off];
+            if constexpr (BF16) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[2 * e] = __builtin_fmaf(w, bf16lo(x[e]), acc[2 * e]);
+                    acc[2 * e + 1] = __builtin_fmaf(w, bf16hi(x[e]), acc[2 * e + 1]);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(w, __uint_as_float(x[e]), acc[e]);
+            }
+        }
+    }
+    u32x4 y;
+    if constexpr (BF16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y[e] = __float_as_uint(acc[e]);
+    }
+    ((u32x4*)a.out)[row * a.chunks + cc] = y;
+    if (a.lse_out && cc == 0) a.lse_out[lidx] = L;
+}
+
+template <bool BF16>
+hipError_t launch_merge(const MergeParams& p, hipStream_t s) {
+    MergeArgs a;
+    for (int r = 0; r < kMaxPartials; ++r) {
+        a.outs[r] = r < p.n ? p.outs[r] : nullptr;
+        a.lses[r] = r < p.n ? p.lses[r] : nullptr;
+    }
+    a.out = p.out;
+    a.lse_out = p.lse_out;
+    a.n = p.n;
+    a.Nq = p.Nq;
+    a.H = p.H;
+    a.chunks = p.D * (BF16 ? 2 : 4) / 16;
+    a.total = (int64_t)p.B * p.Nq * p.H * a.chunks;
+    if (a.total == 0) return hipSuccess;
+    const int64_t blocks = (a.total + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL((merge_kernel<BF16>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+struct UpdateArgs {
+    u32x4* kv;            // buffer base
+    const u32x4* fk;
+    const u32x4* fv;
+    int64_t plane_vecs;   // B * N * H * D * esize / 16
+    int64_t batch_vecs;   // N * H * D * esize / 16
+    int64_t off_vecs;     // off * H * D * esize / 16
+    int64_t slice_vecs;   // len * H * D * esize / 16 (per batch)
+    int B;
+};
+
+// blockIdx.y = plane * B + b; the slice of one (plane, batch) is contiguous.
+__global__ __launch_bounds__(kThreads) void kv_update_kernel(UpdateArgs a) {
+    const int plane = blockIdx.y / a.B, b = blockIdx.y % a.B;
+    const u32x4* src = (plane ? a.fv : a.fk) + (int64_t)b * a.slice_vecs;
+    u32x4* dst = a.kv + plane * a.plane_vecs + (int64_t)b * a.batch_vecs + a.off_vecs;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x; v < a.slice_vecs; v += stride)
+        dst[v] = src[v];
+}
+
+}  // namespace
+
+hipError_t launch_merge_bf16(const MergeParams& p, hipStream_t s) { return launch_merge<true>(p, s); }
+hipError_t launch_merge_f32(const MergeParams& p, hipStream_t s) { return launch_merge<false>(p, s); }
+
+hipError_t launch_kv_update(const UpdateParams& p, hipStream_t s) {
+    const int64_t row_vecs = (int64_t)p.H * p.D * p.esize / 16;
+    UpdateArgs a;
+    a.kv = (u32x4*)p.kv_buf;
+    a.fk = (const u32x4*)p.fresh_k;
+    a.fv = (const u32x4*)p.fresh_v;
+    a.batch_vecs = (int64_t)p.N * row_vecs;
+    a.plane_vecs = (int64_t)p.B * a.batch_vecs;
+    a.off_vecs = (int64_t)p.off * row_vecs;
+    a.slice_vecs = (int64_t)p.len * row_vecs;
+    a.B = p.B;
+    if (a.slice_vecs == 0 || p.B == 0) return hipSuccess;
+    int64_t bx = (a.slice_vecs + kThreads * 4 - 1) / (kThreads * 4);  // ~4 vectors per lane
+    if (bx < 1) bx = 1;
+    if (bx > 65535) bx = 65535;
+    hipLaunchKernelGGL(kv_update_kernel, dim3((unsigned)bx, (unsigned)(2 * p.B)), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace xdit

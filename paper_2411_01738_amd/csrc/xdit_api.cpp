@@ -1,0 +1,270 @@
+// C ABI of the library (declared in include/xdit.h): argument validation,
+// the per-thread stream and error message, and dispatch to the HIP kernels.
+// Every check runs before any HIP call, so a rejected call touches neither the
+// device nor the caller's buffers.
+#include "../../include/xdit.h"
+
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local hipStream_t g_stream = nullptr;
+thread_local char g_error[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof(g_error), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+void clear_error() { g_error[0] = '\0'; }
+
+constexpr int64_t kMaxDim = INT32_MAX;
+
+int esize_of(int32_t dtype) { return dtype == XDIT_BF16 ? 2 : 4; }
+
+int check_dtype_dim(int32_t dtype, int64_t head_dim) {
+    if (dtype != XDIT_BF16 && dtype != XDIT_F32)
+        return fail(XDIT_ERR_DTYPE, "unknown dtype %d (expected XDIT_BF16=0 or XDIT_F32=1)", dtype);
+    if (head_dim != 64 && head_dim != 72 && head_dim != 128)
+        return fail(XDIT_ERR_UNSUPPORTED, "head_dim %lld not supported (64, 72 or 128)",
+                    (long long)head_dim);
+    return XDIT_OK;
+}
+
+int check_dims(const char* what, int64_t B, int64_t n1, int64_t n2, int64_t H) {
+    if (B < 0 || n1 < 0 || n2 < 0 || H < 0)
+        return fail(XDIT_ERR_SHAPE, "%s: negative dimension", what);
+    if (B > kMaxDim || n1 > kMaxDim || n2 > kMaxDim || H > kMaxDim)
+        return fail(XDIT_ERR_SHAPE, "%s: dimension exceeds 2^31-1", what);
+    // keep every tensor below 2^40 elements so offsets never overflow
+    if ((double)B * (double)(n1 > n2 ? n1 : n2) * (double)H * 128.0 > 1099511627776.0)
+        return fail(XDIT_ERR_SHAPE, "%s: tensor too large", what);
+    return XDIT_OK;
+}
+
+// The kernels address each batch's rows with 32-bit byte offsets, plus up to
+// one tile (256 rows) of look-ahead past the end.
+int check_batch_bytes(const char* what, int64_t rows, int64_t heads, int64_t head_dim, int esize) {
+    const int64_t row = heads * head_dim * esize;
+    if ((rows + 256) * row >= ((int64_t)1 << 31))
+        return fail(XDIT_ERR_SHAPE, "%s: one batch of a tensor exceeds 2 GiB", what);
+    return XDIT_OK;
+}
+
+struct Span {
+    const void* p;
+    int64_t bytes;
+    const char* name;
+};
+
+bool overlap(const Span& a, const Span& b) {
+    if (a.bytes <= 0 || b.bytes <= 0) return false;
+    const uintptr_t a0 = (uintptr_t)a.p, b0 = (uintptr_t)b.p;
+    return a0 < b0 + (uintptr_t)b.bytes && b0 < a0 + (uintptr_t)a.bytes;
+}
+
+int check_ptr(const Span& s) {
+    if (s.bytes > 0 && s.p == nullptr) return fail(XDIT_ERR_NULL, "%s is NULL", s.name);
+    if (s.bytes > 0 && ((uintptr_t)s.p & 15u) != 0)
+        return fail(XDIT_ERR_LAYOUT, "%s is not 16-byte aligned", s.name);
+    return XDIT_OK;
+}
+
+int check_no_overlap(const Span& out, const Span& in) {
+    if (overlap(out, in)) return fail(XDIT_ERR_ALIAS, "%s overlaps %s", out.name, in.name);
+    return XDIT_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(XDIT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return XDIT_OK;
+}
+
+#define XDIT_TRY(expr)            \
+    do {                          \
+        const int rc_ = (expr);   \
+        if (rc_ != XDIT_OK) return rc_; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int xdit_set_stream(void* stream) {
+    g_stream = (hipStream_t)stream;
+    return XDIT_OK;
+}
+
+void* xdit_get_stream(void) { return (void*)g_stream; }
+
+const char* xdit_last_error(void) { return g_error; }
+
+const char* xdit_version(void) { return "xdit-mi355x 0.1 (gfx950)"; }
+
+int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, float* lse,
+                    int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
+                    int32_t dtype) {
+    clear_error();
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    XDIT_TRY(check_dims("xdit_chunk_attn", batch, q_len, kv_len, heads));
+    XDIT_TRY(check_batch_bytes("xdit_chunk_attn", q_len > kv_len ? q_len : kv_len, heads, head_dim,
+                               esize_of(dtype)));
+    const int64_t es = esize_of(dtype);
+    const int64_t row = heads * head_dim * es;
+    const Span sq{q, batch * q_len * row, "q"}, sk{k, batch * kv_len * row, "k"},
+        sv{v, batch * kv_len * row, "v"}, so{out, batch * q_len * row, "out"},
+        sl{lse, lse ? batch * heads * q_len * 4 : 0, "lse"};
+    for (const Span* s : {&sq, &sk, &sv, &so}) XDIT_TRY(check_ptr(*s));
+    if (lse && ((uintptr_t)lse & 3u)) return fail(XDIT_ERR_LAYOUT, "lse is not 4-byte aligned");
+    for (const Span* s : {&sq, &sk, &sv}) {
+        XDIT_TRY(check_no_overlap(so, *s));
+        XDIT_TRY(check_no_overlap(sl, *s));
+    }
+    XDIT_TRY(check_no_overlap(sl, so));
+    if (batch == 0 || q_len == 0 || heads == 0) return XDIT_OK;
+
+    xdit::AttnParams p{};
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.out = out;
+    p.lse = lse;
+    p.B = (int)batch;
+    p.H = (int)heads;
+    p.Nq = (int)q_len;
+    p.Nk = (int)kv_len;
+    p.D = (int)head_dim;
+    const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
+                                            : xdit::launch_attn_f32(p, g_stream);
+    return hip_status(e, "xdit_chunk_attn launch");
+}
+
+static int check_patch_args(const char* fn, const void* q, void* kv_buf, int64_t patch_off,
+                            int64_t patch_len, const void* fresh_k, const void* fresh_v,
+                            const void* out, int64_t batch, int64_t seq_len, int64_t heads,
+                            int64_t head_dim, int32_t dtype) {
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    XDIT_TRY(check_dims(fn, batch, seq_len, 0, heads));  // patch_len is bounded by the range check
+    XDIT_TRY(check_batch_bytes(fn, seq_len, heads, head_dim, esize_of(dtype)));
+    if (patch_off < 0 || patch_len < 0 || patch_off > seq_len - patch_len)
+        return fail(XDIT_ERR_RANGE, "%s: slice [%lld, %lld) outside the buffer of %lld rows", fn,
+                    (long long)patch_off, (long long)(patch_off + patch_len), (long long)seq_len);
+    const int64_t row = heads * head_dim * esize_of(dtype);
+    const Span sb{kv_buf, 2 * batch * seq_len * row, "kv_buf"},
+        sk{fresh_k, batch * patch_len * row, "fresh_k"}, sv{fresh_v, batch * patch_len * row, "fresh_v"},
+        sq{q, q ? batch * patch_len * row : 0, "q"}, so{out, out ? batch * patch_len * row : 0, "out"};
+    for (const Span* s : {&sb, &sk, &sv, &sq, &so}) XDIT_TRY(check_ptr(*s));
+    XDIT_TRY(check_no_overlap(sk, sb));
+    XDIT_TRY(check_no_overlap(sv, sb));
+    for (const Span* s : {&sq, &sb, &sk, &sv}) XDIT_TRY(check_no_overlap(so, *s));
+    return XDIT_OK;
+}
+
+int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patch_len,
+                    const void* fresh_k, const void* fresh_v, void* out, int64_t batch,
+                    int64_t seq_len, int64_t heads, int64_t head_dim, int32_t dtype) {
+    clear_error();
+    if (patch_len > 0 && (q == nullptr || out == nullptr))
+        return fail(XDIT_ERR_NULL, "xdit_patch_attn: q and out are required");
+    XDIT_TRY(check_patch_args("xdit_patch_attn", q, kv_buf, patch_off, patch_len, fresh_k,
+                              fresh_v, out, batch, seq_len, heads, head_dim, dtype));
+    if (batch == 0 || patch_len == 0 || heads == 0) return XDIT_OK;
+
+    const int64_t plane = batch * seq_len * heads * head_dim * esize_of(dtype);
+    xdit::AttnParams p{};
+    p.q = q;
+    p.k = kv_buf;
+    p.v = (const char*)kv_buf + plane;
+    p.fresh_k = fresh_k;
+    p.fresh_v = fresh_v;
+    p.wk = kv_buf;
+    p.wv = (char*)kv_buf + plane;
+    p.out = out;
+    p.lse = nullptr;
+    p.B = (int)batch;
+    p.H = (int)heads;
+    p.Nq = (int)patch_len;
+    p.Nk = (int)seq_len;
+    p.D = (int)head_dim;
+    p.off = (int)patch_off;
+    p.len = (int)patch_len;
+    const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
+                                            : xdit::launch_attn_f32(p, g_stream);
+    return hip_status(e, "xdit_patch_attn launch");
+}
+
+int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const void* fresh_k,
+                   const void* fresh_v, int64_t batch, int64_t seq_len, int64_t heads,
+                   int64_t head_dim, int32_t dtype) {
+    clear_error();
+    XDIT_TRY(check_patch_args("xdit_kv_update", nullptr, kv_buf, patch_off, patch_len, fresh_k,
+                              fresh_v, nullptr, batch, seq_len, heads, head_dim, dtype));
+    if (batch == 0 || patch_len == 0 || heads == 0) return XDIT_OK;
+    xdit::UpdateParams p{};
+    p.kv_buf = kv_buf;
+    p.fresh_k = fresh_k;
+    p.fresh_v = fresh_v;
+    p.B = (int)batch;
+    p.N = (int)seq_len;
+    p.H = (int)heads;
+    p.D = (int)head_dim;
+    p.off = (int)patch_off;
+    p.len = (int)patch_len;
+    p.esize = esize_of(dtype);
+    return hip_status(xdit::launch_kv_update(p, g_stream), "xdit_kv_update launch");
+}
+
+int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n, void* out,
+                   float* lse_out, int64_t batch, int64_t q_len, int64_t heads, int64_t head_dim,
+                   int32_t dtype) {
+    clear_error();
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    XDIT_TRY(check_dims("xdit_lse_merge", batch, q_len, 0, heads));
+    XDIT_TRY(check_batch_bytes("xdit_lse_merge", q_len, heads, head_dim, esize_of(dtype)));
+    if (n < 1 || n > XDIT_MAX_PARTIALS)
+        return fail(XDIT_ERR_RANGE, "xdit_lse_merge: n = %d outside [1, %d]", n, XDIT_MAX_PARTIALS);
+    if (outs == nullptr || lses == nullptr)
+        return fail(XDIT_ERR_NULL, "xdit_lse_merge: outs / lses host arrays are NULL");
+    const int64_t obytes = batch * q_len * heads * head_dim * esize_of(dtype);
+    const int64_t lbytes = batch * heads * q_len * 4;
+    const Span so{out, obytes, "out"}, slo{lse_out, lse_out ? lbytes : 0, "lse_out"};
+    XDIT_TRY(check_ptr(so));
+    if (lse_out && ((uintptr_t)lse_out & 3u)) return fail(XDIT_ERR_LAYOUT, "lse_out is not 4-byte aligned");
+    XDIT_TRY(check_no_overlap(slo, so));
+    for (int r = 0; r < n; ++r) {
+        const Span sp{outs[r], obytes, "outs[r]"}, sl{lses[r], lbytes, "lses[r]"};
+        XDIT_TRY(check_ptr(sp));
+        if (lbytes > 0 && lses[r] == nullptr) return fail(XDIT_ERR_NULL, "lses[%d] is NULL", r);
+        if (lbytes > 0 && ((uintptr_t)lses[r] & 3u))
+            return fail(XDIT_ERR_LAYOUT, "lses[%d] is not 4-byte aligned", r);
+        if (outs[r] != out) XDIT_TRY(check_no_overlap(so, sp));  // exact in-place is allowed
+        XDIT_TRY(check_no_overlap(so, sl));
+        XDIT_TRY(check_no_overlap(slo, sl));
+        XDIT_TRY(check_no_overlap(slo, sp));
+    }
+    if (obytes == 0) return XDIT_OK;
+    xdit::MergeParams p{};
+    p.outs = outs;
+    p.lses = lses;
+    p.n = n;
+    p.out = out;
+    p.lse_out = lse_out;
+    p.B = (int)batch;
+    p.Nq = (int)q_len;
+    p.H = (int)heads;
+    p.D = (int)head_dim;
+    const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_merge_bf16(p, g_stream)
+                                            : xdit::launch_merge_f32(p, g_stream);
+    return hip_status(e, "xdit_lse_merge launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+"""Device-resident state of one workload and the calls of one hot-path step.
+
+A step is one pass over every part of the path for one layer:
+  * the PipeFusion patch steps p = 0..M-1 in order over the layer's K/V
+    buffer (each call updates patch p's slice and attends over the buffer;
+    Section 4.1.2), and
+  * the sequence-parallel share: chunk attention of the local query shard
+    against each K/V chunk, then the log-sum-exp merge of the partials
+    (Section 4.1.1).
+Inputs are uploaded once; every per-call operand is its own dense tensor, as
+it would arrive from a projection or a peer, so the timed region holds only
+library calls.  Repeating a step is idempotent: after the first pass the
+buffer is all fresh and each patch step rewrites the same rows.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import xdit_chunk_attn, xdit_lse_merge, xdit_patch_attn
+from .inputs import Tensors, Workload
+
+
+class HotPath:
+    def __init__(self, w: Workload, t: Tensors, device: str = "cuda"):
+        import torch
+
+        self.w = w
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.dt = dt
+
+        def up(x):
+            return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(device).to(dt)
+
+        B, H, d = w.B, w.H, w.d
+        # K/V buffer at the start of a diffusion step: stale image rows,
+        # fresh text rows
+        self.kv_stale = up(np.stack([t.k_stale, t.v_stale]))
+        self.kv_buf = self.kv_stale.clone()
+        self.patch_q, self.patch_k, self.patch_v, self.patch_out = [], [], [], []
+        for off, ln in w.patches():
+            self.patch_q.append(up(t.q[:, off:off + ln]))
+            self.patch_k.append(up(t.k_fresh[:, off:off + ln]))
+            self.patch_v.append(up(t.v_fresh[:, off:off + ln]))
+            self.patch_out.append(torch.empty((B, ln, H, d), device=device, dtype=dt))
+        self.sp_q = self.sp_out = self.sp_lse = None
+        self.chunk_k, self.chunk_v, self.chunk_out, self.chunk_lse = [], [], [], []
+        if w.sp_chunks:
+            q0, q1 = w.sp_q
+            nq = q1 - q0
+            self.sp_q = up(t.q[:, q0:q1])
+            for s, e in w.sp_chunks:
+                self.chunk_k.append(up(t.k_fresh[:, s:e]))
+                self.chunk_v.append(up(t.v_fresh[:, s:e]))
+                self.chunk_out.append(torch.empty((B, nq, H, d), device=device, dtype=dt))
+                self.chunk_lse.append(torch.empty((B, H, nq), device=device, dtype=torch.float32))
+            self.sp_out = torch.empty((B, nq, H, d), device=device, dtype=dt)
+            self.sp_lse = torch.empty((B, H, nq), device=device, dtype=torch.float32)
+
+    # -- calls ---------------------------------------------------------------
+    def reset_buffer(self) -> None:
+        self.kv_buf.copy_(self.kv_stale)
+
+    def patch_step(self, p: int) -> None:
+        off, ln = self.w.patches()[p]
+        xdit_patch_attn(self.patch_q[p], self.kv_buf, off, ln, self.patch_k[p], self.patch_v[p],
+                        self.patch_out[p])
+
+    def chunk_step(self, r: int) -> None:
+        xdit_chunk_attn(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
+                        self.chunk_lse[r])
+
+    def merge(self) -> None:
+        n = len(self.chunk_out)
+        xdit_lse_merge(self.chunk_out, self.chunk_lse, n, self.sp_out, self.sp_lse)
+
+    def step(self) -> None:
+        for p in range(len(self.patch_q)):
+            self.patch_step(p)
+        if self.sp_q is not None:
+            for r in range(len(self.chunk_k)):
+                self.chunk_step(r)
+            self.merge()
+
+    # -- accounting ----------------------------------------------------------
+    def patch_flops(self, p: int) -> float:
+        return self.w.attn_flops(self.w.patches()[p][1], self.w.N)
+
+    def chunk_flops(self, r: int) -> float:
+        s, e = self.w.sp_chunks[r]
+        return self.w.attn_flops(self.w.sp_q[1] - self.w.sp_q[0], e - s)
+
+    def step_flops(self) -> float:
+        f = sum(self.patch_flops(p) for p in range(len(self.patch_q)))
+        if self.sp_q is not None:
+            f += sum(self.chunk_flops(r) for r in range(len(self.chunk_k)))
+        return f
+
+    def merge_bytes(self) -> float:
+        """n partials (O and LSE) read, merged O and LSE written."""
+        w = self.w
+        nq = w.sp_q[1] - w.sp_q[0]
+        n = len(w.sp_chunks)
+        o = w.B * nq * w.H * w.d * w.esize
+        lse = 4 * w.B * w.H * nq
+        return n * (o + lse) + o + lse
+
+    def update_bytes(self, p: int) -> float:
+        """K and V slice: read from the fresh tensors and written to the buffer."""
+        w = self.w
+        ln = w.patches()[p][1]
+        return 2 * 2 * w.B * ln * w.H * w.d * w.esize

@@ -43,6 +43,8 @@ class Workload:
     def patches(self):
         """(offset, length) of the M patches: near-equal contiguous splits of
         the image rows, the first (n_img mod M) patches one row longer."""
+        if self.M == 0:
+            return []
         base, extra = divmod(self.n_img, self.M)
         out, off = [], 0
         for p in range(self.M):
@@ -79,7 +81,7 @@ WORKLOADS = {
                        note="Pixart 1024px: 128x128 latent, 2x2 patchify, CFG pair"),
     "sd3": Workload("sd3", "bf16", 2, 24, 64, 4096, 333, 8, 2,
                     note="SD3 joint attention: 4096 image + 333 text tokens"),
-    "flux": Workload("flux", "bf16", 1, 24, 128, 16384, 512, 4, 3,
+    "flux": Workload("flux", "bf16", 1, 24, 128, 16384, 512, 0, 3,
                      sp_q=(0, 4224), sp_chunks=_even_chunks(16896, 4),
                      note="Flux 2048px sequence-parallel share: 4 shards of 4096 image"
                           " + 128 text tokens; Q is shard 0"),

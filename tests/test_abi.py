@@ -1,0 +1,135 @@
+"""CPU checks of the C-ABI library: it loads, exports every entry point the
+public header declares, and rejects bad arguments before touching the device.
+
+The rejection tests pass fake device addresses that are never dereferenced:
+every call has an argument that validation must reject.  They are skipped
+where a GPU is visible, so that a validation bug can never turn into a launch
+on fake pointers."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2411_01738_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "xdit.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(xdit_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = header_functions()
+    for fn in ["xdit_patch_attn", "xdit_chunk_attn", "xdit_lse_merge", "xdit_kv_update",
+               "xdit_set_stream", "xdit_get_stream", "xdit_last_error", "xdit_version"]:
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.lib()
+    for name in header_functions():
+        assert hasattr(lib, name), f"{name} declared in xdit.h but not exported"
+    assert set(_lib.SIGNATURES) == set(header_functions())
+
+
+def test_version_and_stream_roundtrip():
+    lib = _lib.lib()
+    assert b"gfx950" in lib.xdit_version()
+    assert lib.xdit_set_stream(0x1234) == 0
+    assert lib.xdit_get_stream() == 0x1234
+    assert lib.xdit_set_stream(None) == 0
+    assert lib.xdit_get_stream() in (None, 0)
+
+
+def _gpu_visible() -> bool:
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+needs_no_gpu = pytest.mark.skipif(_gpu_visible(), reason="fake-pointer checks run only without a GPU")
+
+A = 0x7F0000000000  # fake, 16-byte aligned device addresses, far apart
+MB = 1 << 24
+
+
+def P(i):
+    return A + i * (1 << 32)
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("case,code", [
+    # (callable on lib, expected status)
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(4), 1, 16, 16, 2, 64, 7), -2),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(4), 1, 16, 16, 2, 80, 0), -7),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(4), -1, 16, 16, 2, 64, 0), -3),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(4), 1, 1 << 31, 16, 2, 64, 0), -3),
+    (lambda L: L.xdit_chunk_attn(None, P(1), P(2), P(3), P(4), 1, 16, 16, 2, 64, 0), -1),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), None, P(4), 1, 16, 16, 2, 64, 0), -1),
+    (lambda L: L.xdit_chunk_attn(P(0) + 8, P(1), P(2), P(3), P(4), 1, 16, 16, 2, 64, 0), -5),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(0) + 64, P(4), 1, 16, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(2), 1, 16, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(3) + 16, 1, 16, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 10, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), -1, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 0, -8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),
+    (lambda L: L.xdit_patch_attn(None, P(1), 0, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -1),
+    (lambda L: L.xdit_patch_attn(P(0), None, 0, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -1),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(1) + 1024, P(3), P(4), 1, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(1), 1, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(0), 1, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(4), 1, 16, 2, 72, 3), -2),
+    (lambda L: L.xdit_kv_update(P(1), 9, 8, P(2), P(3), 1, 16, 2, 64, 0), -4),
+    (lambda L: L.xdit_kv_update(P(1), 0, 8, P(2) + 4, P(3), 1, 16, 2, 64, 0), -5),
+    (lambda L: L.xdit_kv_update(P(1), 0, 8, P(2), P(1) + 2 * 16 * 128 * 2 - 16, 1, 16, 2, 64, 0), -6),
+])
+def test_rejections(case, code):
+    lib = _lib.lib()
+    assert case(lib) == code
+    assert lib.xdit_last_error().decode(), "no message for a rejected call"
+
+
+@needs_no_gpu
+def test_merge_rejections():
+    lib = _lib.lib()
+    arr = ctypes.c_void_p * 65
+    outs = arr(*[P(10 + r) for r in range(65)])
+    lses = arr(*[P(100 + r) for r in range(65)])
+    args = (1, 16, 2, 64, 0)
+    assert lib.xdit_lse_merge(outs, lses, 0, P(5), P(6), *args) == -4
+    assert lib.xdit_lse_merge(outs, lses, 65, P(5), P(6), *args) == -4
+    assert lib.xdit_lse_merge(None, lses, 2, P(5), P(6), *args) == -1
+    assert lib.xdit_lse_merge(outs, lses, 2, P(5), P(100), *args) == -6  # lse_out on a partial's lse
+    assert lib.xdit_lse_merge(outs, lses, 2, P(10) + 16, None, *args) == -6  # shifted overlap
+    assert lib.xdit_lse_merge(outs, lses, 2, P(5), P(6) + 2, *args) == -5
+    bad = arr(P(10), None)
+    assert lib.xdit_lse_merge(bad, lses, 2, P(5), None, *args) == -1
+    assert lib.xdit_lse_merge(outs, lses, 2, P(5), None, 1, 16, 2, 96, 0) == -7
+
+
+@needs_no_gpu
+def test_empty_calls_succeed_without_launching():
+    lib = _lib.lib()
+    assert lib.xdit_chunk_attn(None, None, None, None, None, 1, 0, 0, 2, 64, 0) == 0
+    assert lib.xdit_patch_attn(None, P(1), 16, 0, None, None, None, 1, 16, 2, 64, 0) == 0
+    assert lib.xdit_kv_update(P(1), 3, 0, None, None, 1, 16, 2, 128, 1) == 0
+    assert lib.xdit_last_error().decode() == ""
+
+
+def test_product_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2411_01738_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, re.M), f
+                assert "xdit_oracle" not in text and "liboracle" not in text, f

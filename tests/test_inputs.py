@@ -1,0 +1,47 @@
+"""Input generation: bf16 rounding, determinism and workload geometry."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2411_01738_amd.inputs import WORKLOADS, bf16_round, generate, random_io
+
+
+def test_bf16_round_matches_torch_rne():
+    x = np.random.Generator(np.random.PCG64(1)).standard_normal(100000, dtype=np.float32) * 3
+    # exact ties: halfway between two bf16 values
+    ties = (np.arange(1, 200, dtype=np.uint32) << 16 | np.uint32(0x8000)).view(np.float32)
+    x = np.concatenate([x, ties, -ties, np.float32([0.0, -0.0, 1e-30, 65504.0])])
+    ref = torch.from_numpy(x).to(torch.bfloat16).float().numpy()
+    assert np.array_equal(bf16_round(x), ref)
+
+
+def test_generation_is_deterministic_and_exact_in_bf16():
+    w = WORKLOADS["sd3"]
+    a = random_io((2, 3, 4, 8), "bf16", 9)
+    assert np.array_equal(a, random_io((2, 3, 4, 8), "bf16", 9))
+    assert np.array_equal(bf16_round(a), a)
+
+
+def test_stale_rows_only_on_image_tokens():
+    w = WORKLOADS["tiny"]
+    t = generate(w)
+    assert t.q.shape == (w.B, w.N, w.H, w.d)
+    diff = np.abs(t.k_stale - t.k_fresh)
+    assert 0.02 < diff.mean() < 0.06  # N(0, 0.05^2) noise: mean |x| = 0.05*sqrt(2/pi)
+
+
+def test_workload_geometry():
+    cog = WORKLOADS["cog"]
+    lens = [ln for _, ln in cog.patches()]
+    assert lens == [1097] * 14 + [1096] * 2 and sum(lens) == 17550 and cog.N == 17776
+    offs = [o for o, _ in cog.patches()]
+    assert offs[0] == 0 and all(offs[i + 1] == offs[i] + lens[i] for i in range(15))
+    assert WORKLOADS["cog"].sp_chunks == tuple((2222 * r, 2222 * (r + 1)) for r in range(8))
+    flux = WORKLOADS["flux"]
+    assert flux.N == 16896 and flux.sp_q == (0, 4224) and len(flux.sp_chunks) == 4
+    assert all(e - s == 4224 for s, e in flux.sp_chunks)
+    sd3 = WORKLOADS["sd3"]
+    assert sd3.N == 4429 and [ln for _, ln in sd3.patches()] == [512] * 8
+    px = WORKLOADS["pixart"]
+    assert px.attn_flops(1024, 4096) == 4 * 2 * 16 * 1024 * 4096 * 72

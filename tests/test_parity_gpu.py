@@ -1,0 +1,278 @@
+"""GPU parity of the HIP path against the fp64 oracle, element by element, at
+sizes the oracle finishes in seconds that span several tiles and ragged
+tails, plus the edge cases.  Every call goes through the C ABI."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2411_01738_amd as xd
+from paper_2411_01738_amd.inputs import WORKLOADS, generate, random_io
+from tests.gpu_util import check_lse, check_out, tdtype, to_gpu, to_np, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.get()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    return torch_mod()
+
+
+def _empty_out(torch, B, Nq, H, d, dtype):
+    # NaN-filled so that rows the kernel fails to write are caught
+    return torch.full((B, Nq, H, d), float("nan"), device="cuda", dtype=tdtype(dtype))
+
+
+def _lse_buf(torch, B, H, Nq):
+    return torch.full((B, H, Nq), float("nan"), device="cuda", dtype=torch.float32)
+
+
+# ---------------------------------------------------------------------------
+# chunk attention (O and LSE)
+# ---------------------------------------------------------------------------
+CHUNK_CASES = [
+    # dtype, B, Nq, Nk, H, d
+    ("bf16", 2, 200, 333, 3, 64),
+    ("bf16", 1, 130, 257, 2, 72),
+    ("bf16", 2, 129, 190, 2, 128),
+    ("bf16", 1, 1, 1, 1, 64),
+    ("bf16", 1, 5, 64, 1, 72),
+    ("bf16", 1, 128, 128, 1, 128),
+    ("f32", 1, 256, 256, 2, 64),
+    ("f32", 2, 70, 97, 3, 72),
+    ("f32", 1, 65, 33, 2, 128),
+]
+
+
+@pytest.mark.parametrize("dtype,B,Nq,Nk,H,d", CHUNK_CASES)
+def test_chunk_attn(orc, torch, dtype, B, Nq, Nk, H, d):
+    seed = B * 1000003 + Nq * 101 + Nk * 7 + d
+    q = random_io((B, Nq, H, d), dtype, seed)
+    k = random_io((B, Nk, H, d), dtype, seed + 1)
+    v = random_io((B, Nk, H, d), dtype, seed + 2)
+    ref_o, ref_l = orc.attention(q, k, v)
+    out = _empty_out(torch, B, Nq, H, d, dtype)
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_chunk_attn(to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype), out, lse)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, dtype, "chunk out")
+    check_lse(to_np(lse), ref_l, dtype, "chunk lse")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("d", [64, 72, 128])
+def test_chunk_empty_kv(torch, dtype, d):
+    B, Nq, H = 1, 70, 2
+    q = to_gpu(random_io((B, Nq, H, d), dtype, 5), dtype)
+    e = torch.zeros((B, 0, H, d), device="cuda", dtype=tdtype(dtype))
+    out = _empty_out(torch, B, Nq, H, d, dtype)
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_chunk_attn(q, e, e, out, lse)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0).item()
+    assert torch.all(torch.isneginf(lse)).item()
+
+
+def test_chunk_empty_q_is_noop(torch):
+    q = torch.zeros((1, 0, 2, 64), device="cuda", dtype=torch.bfloat16)
+    k = to_gpu(random_io((1, 10, 2, 64), "bf16", 3), "bf16")
+    out = torch.zeros((1, 0, 2, 64), device="cuda", dtype=torch.bfloat16)
+    xd.xdit_chunk_attn(q, k, k.clone(), out, None)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("d", [64, 72, 128])
+def test_constant_values_give_constant_output(torch, d):
+    """Softmax rows sum to one: V rows all equal c gives O = c (up to the bf16
+    rounding of c itself, which is exact here)."""
+    B, Nq, Nk, H = 1, 150, 300, 2
+    q = to_gpu(random_io((B, Nq, H, d), "bf16", 8), "bf16")
+    k = to_gpu(random_io((B, Nk, H, d), "bf16", 9), "bf16")
+    crow = random_io((B, 1, H, d), "bf16", 10)
+    v = to_gpu(np.broadcast_to(crow, (B, Nk, H, d)).copy(), "bf16")
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    xd.xdit_chunk_attn(q, k, v, out, None)
+    torch.cuda.synchronize()
+    c = np.broadcast_to(crow, (B, Nq, H, d))
+    err = np.abs(to_np(out) - c)
+    # O = c * sum(bf16(p)) / sum(p), then rounded to bf16: two relative
+    # roundings of at most 2^-9 each
+    assert np.all(err <= 2 * 2.0 ** -9 * np.abs(c) * 1.01 + 1e-7), err.max()
+
+
+# ---------------------------------------------------------------------------
+# LSE merge
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 72), ("bf16", 128), ("f32", 64),
+                                     ("f32", 128)])
+def test_chunks_then_merge_equal_full(orc, torch, dtype, d):
+    B, Nq, Nk, H = 2, 150, 500, 2
+    q = random_io((B, Nq, H, d), dtype, 20 + d)
+    k = random_io((B, Nk, H, d), dtype, 21 + d)
+    v = random_io((B, Nk, H, d), dtype, 22 + d)
+    ref_o, ref_l = orc.attention(q, k, v)
+    bounds = [(0, 64), (64, 64), (64, 200), (200, 201), (201, 500)]  # uneven, with an empty chunk
+    qg = to_gpu(q, dtype)
+    outs, lses = [], []
+    for s, e in bounds:
+        o = _empty_out(torch, B, Nq, H, d, dtype)
+        l = _lse_buf(torch, B, H, Nq)
+        xd.xdit_chunk_attn(qg, to_gpu(k[:, s:e], dtype), to_gpu(v[:, s:e], dtype), o, l)
+        outs.append(o)
+        lses.append(l)
+    out = _empty_out(torch, B, Nq, H, d, dtype)
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_lse_merge(outs, lses, len(outs), out, lse)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, dtype, "merged out vs full")
+    check_lse(to_np(lse), ref_l, dtype, "merged lse vs full")
+    # merge alone: the oracle merges the GPU's own partials
+    mo, ml = orc.merge([to_np(o) for o in outs], [to_np(l) for l in lses])
+    check_out(to_np(out), mo, dtype, "merge vs oracle merge")
+    check_lse(to_np(lse), ml, dtype, "merge lse vs oracle merge")
+
+
+def test_merge_single_partial_is_copy(torch):
+    B, Nq, H, d = 1, 77, 3, 72
+    o = to_gpu(random_io((B, Nq, H, d), "bf16", 30), "bf16")
+    l = torch.from_numpy(random_io((B, H, Nq), "f32", 31)).cuda()
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_lse_merge([o], [l], 1, out, lse)
+    torch.cuda.synchronize()
+    assert torch.equal(out, o)
+    assert torch.equal(lse, l)
+
+
+def test_merge_in_place_and_all_empty(torch):
+    B, Nq, H, d = 1, 40, 2, 64
+    parts = [to_gpu(random_io((B, Nq, H, d), "bf16", 40 + r), "bf16") for r in range(3)]
+    ninf = [torch.full((B, H, Nq), float("-inf"), device="cuda") for _ in range(3)]
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_lse_merge(parts, ninf, 3, out, lse)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0).item() and torch.all(torch.isneginf(lse)).item()
+    # in place into partial 0, partial 1 empty
+    lses = [torch.zeros((B, H, Nq), device="cuda"), ninf[1], torch.zeros((B, H, Nq), device="cuda")]
+    expect = ((parts[0].float() + parts[2].float()) / 2).to(torch.bfloat16)
+    xd.xdit_lse_merge(parts, lses, 3, parts[0], None)
+    torch.cuda.synchronize()
+    assert torch.equal(parts[0], expect)
+
+
+# ---------------------------------------------------------------------------
+# PipeFusion patch step
+# ---------------------------------------------------------------------------
+PATCH_CASES = [
+    # dtype, B, N, H, d, patches (offset, length) applied in order
+    ("bf16", 2, 300, 2, 64, [(37, 150), (0, 37), (187, 113)]),
+    ("bf16", 1, 257, 3, 72, [(0, 64), (64, 129), (193, 64)]),
+    ("bf16", 1, 200, 2, 128, [(100, 100), (0, 100)]),
+    ("f32", 1, 256, 2, 64, [(0, 64), (64, 64), (128, 64), (192, 64)]),
+    ("f32", 2, 150, 2, 72, [(50, 33), (83, 67)]),
+    ("f32", 1, 97, 2, 128, [(1, 95)]),
+]
+
+
+@pytest.mark.parametrize("dtype,B,N,H,d,patches", PATCH_CASES)
+def test_patch_steps_sequential(orc, torch, dtype, B, N, H, d, patches):
+    seed = 7000 + N + d
+    q = random_io((B, N, H, d), dtype, seed)
+    kf = random_io((B, N, H, d), dtype, seed + 1)
+    vf = random_io((B, N, H, d), dtype, seed + 2)
+    ks = random_io((B, N, H, d), dtype, seed + 3)
+    vs = random_io((B, N, H, d), dtype, seed + 4)
+    kv_ref = np.ascontiguousarray(np.stack([ks, vs]))
+    kv = to_gpu(kv_ref, dtype)
+    for off, ln in patches:
+        sl = slice(off, off + ln)
+        ref_o, _ = orc.patch(q[:, sl].copy(), kv_ref, off, kf[:, sl].copy(), vf[:, sl].copy())
+        out = _empty_out(torch, B, ln, H, d, dtype)
+        xd.xdit_patch_attn(to_gpu(q[:, sl], dtype), kv, off, ln, to_gpu(kf[:, sl], dtype),
+                           to_gpu(vf[:, sl], dtype), out)
+        torch.cuda.synchronize()
+        check_out(to_np(out), ref_o, dtype, f"patch ({off},{ln}) out")
+        assert np.array_equal(to_np(kv), kv_ref), f"patch ({off},{ln}): buffer not bit-exact"
+
+
+def test_patch_reads_fresh_rows_not_the_buffer(orc, torch):
+    """The own slice of the buffer holds NaN before the step: every workgroup
+    must take those rows from the fresh K/V, never from the buffer."""
+    B, N, H, d, off, ln = 1, 256, 2, 64, 64, 128
+    q = random_io((B, ln, H, d), "bf16", 50)
+    kf = random_io((B, ln, H, d), "bf16", 51)
+    vf = random_io((B, ln, H, d), "bf16", 52)
+    kv_ref = np.stack([random_io((B, N, H, d), "bf16", 53), random_io((B, N, H, d), "bf16", 54)])
+    kv_ref = np.ascontiguousarray(kv_ref)
+    poisoned = kv_ref.copy()
+    poisoned[:, :, off:off + ln] = np.nan
+    kv = to_gpu(poisoned, "bf16")
+    ref_o, _ = orc.patch(q, kv_ref, off, kf, vf)
+    out = _empty_out(torch, B, ln, H, d, "bf16")
+    xd.xdit_patch_attn(to_gpu(q, "bf16"), kv, off, ln, to_gpu(kf, "bf16"), to_gpu(vf, "bf16"), out)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, "bf16", "poisoned-slice patch out")
+    assert np.array_equal(to_np(kv), kv_ref)
+
+
+def test_patch_idempotent_and_empty(torch):
+    B, N, H, d = 1, 192, 2, 72
+    kv0 = np.ascontiguousarray(np.stack([random_io((B, N, H, d), "bf16", 60),
+                                         random_io((B, N, H, d), "bf16", 61)]))
+    kv = to_gpu(kv0, "bf16")
+    q = to_gpu(random_io((B, 64, H, d), "bf16", 62), "bf16")
+    fk = to_gpu(random_io((B, 64, H, d), "bf16", 63), "bf16")
+    fv = to_gpu(random_io((B, 64, H, d), "bf16", 64), "bf16")
+    o1 = _empty_out(torch, B, 64, H, d, "bf16")
+    o2 = _empty_out(torch, B, 64, H, d, "bf16")
+    xd.xdit_patch_attn(q, kv, 64, 64, fk, fv, o1)
+    snap = kv.clone()
+    xd.xdit_patch_attn(q, kv, 64, 64, fk, fv, o2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(kv, snap)
+    e = torch.zeros((B, 0, H, d), device="cuda", dtype=torch.bfloat16)
+    xd.xdit_patch_attn(e, kv, N, 0, e, e, e)
+    torch.cuda.synchronize()
+    assert torch.equal(kv, snap)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_kv_update_exact(torch, dtype):
+    B, N, H, d = 2, 333, 3, 72
+    kv0 = np.ascontiguousarray(np.stack([random_io((B, N, H, d), dtype, 70),
+                                         random_io((B, N, H, d), dtype, 71)]))
+    kv = to_gpu(kv0, dtype)
+    off, ln = 101, 77
+    fk = random_io((B, ln, H, d), dtype, 72)
+    fv = random_io((B, ln, H, d), dtype, 73)
+    xd.xdit_kv_update(kv, off, ln, to_gpu(fk, dtype), to_gpu(fv, dtype))
+    torch.cuda.synchronize()
+    exp = kv0.copy()
+    exp[0, :, off:off + ln] = fk
+    exp[1, :, off:off + ln] = fv
+    assert np.array_equal(to_np(kv), exp)
+
+
+def test_patch_all_fresh_equals_chunk_attention(torch):
+    """A patch step over an all-fresh buffer is plain attention of the patch's
+    queries; the GPU's two entry points agree bit for bit."""
+    w = WORKLOADS["tiny"]
+    t = generate(w)
+    kv = to_gpu(np.ascontiguousarray(np.stack([t.k_fresh, t.v_fresh])), "f32")
+    k, v = to_gpu(t.k_fresh, "f32"), to_gpu(t.v_fresh, "f32")
+    for off, ln in w.patches():
+        q = to_gpu(t.q[:, off:off + ln], "f32")
+        o1 = _empty_out(torch, w.B, ln, w.H, w.d, "f32")
+        o2 = _empty_out(torch, w.B, ln, w.H, w.d, "f32")
+        xd.xdit_patch_attn(q, kv, off, ln, k[:, off:off + ln].contiguous(),
+                           v[:, off:off + ln].contiguous(), o1)
+        xd.xdit_chunk_attn(q, k, v, o2, None)
+        torch.cuda.synchronize()
+        assert torch.equal(o1, o2)
