@@ -24,6 +24,17 @@ def torch():
     return torch_mod()
 
 
+@pytest.fixture(params=["auto", "wide", "narrow"])
+def tile_shape(request, monkeypatch):
+    """Workgroup shape of the bf16 kernel: 128 query rows x 2 key splits
+    ("wide"), 64 x 4 ("narrow"), or the library's own choice."""
+    if request.param == "auto":
+        monkeypatch.delenv("XDIT_ATTN_TILE", raising=False)
+    else:
+        monkeypatch.setenv("XDIT_ATTN_TILE", request.param)
+    return request.param
+
+
 def _empty_out(torch, B, Nq, H, d, dtype):
     # NaN-filled so that rows the kernel fails to write are caught
     return torch.full((B, Nq, H, d), float("nan"), device="cuda", dtype=tdtype(dtype))
@@ -51,7 +62,7 @@ CHUNK_CASES = [
 
 
 @pytest.mark.parametrize("dtype,B,Nq,Nk,H,d", CHUNK_CASES)
-def test_chunk_attn(orc, torch, dtype, B, Nq, Nk, H, d):
+def test_chunk_attn(orc, torch, tile_shape, dtype, B, Nq, Nk, H, d):
     seed = B * 1000003 + Nq * 101 + Nk * 7 + d
     q = random_io((B, Nq, H, d), dtype, seed)
     k = random_io((B, Nk, H, d), dtype, seed + 1)
@@ -111,7 +122,7 @@ def test_constant_values_give_constant_output(torch, d):
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 72), ("bf16", 128), ("f32", 64),
                                      ("f32", 128)])
-def test_chunks_then_merge_equal_full(orc, torch, dtype, d):
+def test_chunks_then_merge_equal_full(orc, torch, tile_shape, dtype, d):
     B, Nq, Nk, H = 2, 150, 500, 2
     q = random_io((B, Nq, H, d), dtype, 20 + d)
     k = random_io((B, Nk, H, d), dtype, 21 + d)
@@ -182,7 +193,7 @@ PATCH_CASES = [
 
 
 @pytest.mark.parametrize("dtype,B,N,H,d,patches", PATCH_CASES)
-def test_patch_steps_sequential(orc, torch, dtype, B, N, H, d, patches):
+def test_patch_steps_sequential(orc, torch, tile_shape, dtype, B, N, H, d, patches):
     seed = 7000 + N + d
     q = random_io((B, N, H, d), dtype, seed)
     kf = random_io((B, N, H, d), dtype, seed + 1)
@@ -202,7 +213,7 @@ def test_patch_steps_sequential(orc, torch, dtype, B, N, H, d, patches):
         assert np.array_equal(to_np(kv), kv_ref), f"patch ({off},{ln}): buffer not bit-exact"
 
 
-def test_patch_reads_fresh_rows_not_the_buffer(orc, torch):
+def test_patch_reads_fresh_rows_not_the_buffer(orc, torch, tile_shape):
     """The own slice of the buffer holds NaN before the step: every workgroup
     must take those rows from the fresh K/V, never from the buffer."""
     B, N, H, d, off, ln = 1, 256, 2, 64, 64, 128
