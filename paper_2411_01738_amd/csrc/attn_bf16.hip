@@ -14,13 +14,15 @@
 //     that split every K/V tile between them (each takes KW keys of the
 //     BN = KS*KW-key tile).  The KS waves of a query block keep separate
 //     running (max, sum, output) and are merged through LDS at the end, like
-//     the chunk partials of the sequence-parallel merge.  Two or more waves
-//     per SIMD let one wave's matrix work overlap another's softmax;
-//   * K/V tiles are staged through LDS (double buffered, one barrier per
-//     tile); the global loads of tile t+1 are in flight while tile t is
-//     computed.  Loads go through buffer resources: a row past the end, or a
-//     row served by the other source in patch mode, gets an out-of-range
-//     offset and reads as zero, so no lane branches;
+//     the chunk partials of the sequence-parallel merge.  Two waves per SIMD
+//     let one wave's matrix work overlap another's softmax;
+//   * K/V tiles go from memory straight into LDS (buffer loads with an LDS
+//     destination: no registers, no LDS store instructions), NSTAGE tiles
+//     deep, so the loads of the next tiles are in flight while tile t is
+//     computed; one barrier per tile.  A row past the end of its source reads
+//     as zero.  Both tiles are stored row-major as loaded, 16-byte chunks
+//     XOR-swizzled by row where a row has a power-of-two chunk count, so the
+//     operand reads below are free of bank conflicts;
 //   * scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: A = K rows from LDS, B = the wave's Q rows
 //     held in registers for the whole sweep.  In the 32x32 accumulator layout
@@ -34,14 +36,14 @@
 //     depend on when rescales happen;
 //   * O^T = V^T P^T on the same instruction: P^T comes straight from the
 //     score accumulators (no data movement) because the K index order of an
-//     MFMA contraction is free as long as A and B agree; V is transposed into
-//     LDS while staging, with the key order permuted to match P's register
-//     order, so each A operand is one 16-byte LDS read;
-//   * where the output rows are padded (d = 72 -> 96), one padding row of V^T
-//     holds ones, so the same MFMA also produces the row sums of the bf16
-//     weights (the exact normaliser of the bf16 numerator);
-//   * LDS pitches are padded so the 16-byte operand reads of 16 lanes hit
-//     distinct bank groups.
+//     MFMA contraction is free as long as A and B agree; the V^T operand is
+//     read from the row-major V tile with ds_read_b64_tr_b16, which hands
+//     each lane one head dimension of four keys, the keys chosen to match
+//     P's register order;
+//   * where the output rows are padded (d = 72 -> 96), the padding lanes read
+//     a constant chunk in LDS: dimension 72 reads ones, so the same MFMA
+//     also produces the row sums of the bf16 weights (the exact normaliser
+//     of the bf16 numerator), the rest read zeros.
 // Workgroups are renumbered so that all query tiles of one (batch, head) run
 // on the same XCD and share its L2 for K/V (the hardware deals workgroup ids
 // round-robin over the 8 XCDs).
@@ -58,10 +60,15 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr uint32_t kOOB = 0x80000000u;  // offset past any buffer's range: reads 0, writes dropped
 constexpr int kRsrcFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kRescaleLog2 = 8.0f;    // raise the reference max only beyond 2^8 growth
+constexpr int kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
 
 template <int D, int QB_, int KS_, int KW_>
 struct Cfg {
@@ -75,24 +82,29 @@ struct Cfg {
     static constexpr int KSTEPS = DK / 16;
     static constexpr int DBLK = DV / 32;
     static constexpr int CH = D / 8;                 // 16-byte chunks per K/V row
-    static constexpr int KP = DK + 8;                // K tile row pitch (elements)
-    static constexpr int VP = BN + 8;                // V^T tile row pitch (elements)
-    static constexpr int K_ELEMS = BN * KP;
-    static constexpr int V_ELEMS = DV * VP;
-    static constexpr int STAGE = K_ELEMS + V_ELEMS;
-    static constexpr int K_CHUNKS = BN * CH;
-    static constexpr int K_LOADS = (K_CHUNKS + THREADS - 1) / THREADS;
-    static constexpr int V_BLOCKS = (BN / 4) * CH;   // 4 rows x 8 dims per block
-    static constexpr int V_LOADS = (V_BLOCKS + THREADS - 1) / THREADS;
+    static constexpr int ROWB = 16 * CH;             // bytes per row in LDS
+    static constexpr bool SWZ = (CH & (CH - 1)) == 0;  // XOR-swizzle chunks by row
+    static constexpr int SWZ_MASK = SWZ ? (CH < 8 ? CH - 1 : 7) : 0;
+    static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
+    static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
+    static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
+    static constexpr int NSTAGE = kLdsBytes / STAGE_BYTES >= 3 ? 3 : 2;
+    static constexpr int DMA_PER_TILE = TILE_BYTES / 1024;  // 64 lanes x 16 bytes per load
+    static constexpr int DMA_PER_WAVE = (DMA_PER_TILE + NW - 1) / NW;
+    static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = DV > D;      // a padding row of V^T holds ones
     // end-of-sweep exchange: one slot (m, l, O^T accumulators) per partial wave
-    static constexpr int XSLOT = 64 * (2 + 16 * DBLK);         // floats
-    static constexpr int X_ELEMS = 2 * QB * (KS - 1) * XSLOT;  // in 2-byte units
-    static constexpr int LDS_ELEMS = 2 * STAGE > X_ELEMS ? 2 * STAGE : X_ELEMS;
+    static constexpr int XSLOT = 64 * (2 + 16 * DBLK);  // floats
+    static constexpr int X_BYTES = 4 * QB * (KS - 1) * XSLOT;
+    static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES > X_BYTES ? NSTAGE * STAGE_BYTES : X_BYTES;
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
+    static_assert(DV - D == 0 || DV - D == 24, "V padding handled for d = 72 only");
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
+    static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads");
+    static_assert(DMA_PER_TILE >= NW, "every wave loads part of each tile");
+    static_assert(LDS_BYTES <= kLdsBytes, "LDS budget");
 };
 
 struct Args {
@@ -120,18 +132,24 @@ __device__ __forceinline__ u32x4 bload(Rsrc r, uint32_t off) {
 __device__ __forceinline__ void bstore(Rsrc r, uint32_t off, u32x4 x) {
     __builtin_amdgcn_raw_buffer_store_b128(x, r, off, 0, 0);
 }
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes
+// land at dst + 16*l (dst must be the same in every lane).
+__device__ __forceinline__ void dma16(Rsrc r, void* dst, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, off, 0, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (LDS and export counters left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 __device__ __forceinline__ int xcd_remap(int pid, int total) {
     const int per = total >> 3, rem = total & 7;
     const int xcd = pid & 7, loc = pid >> 3;
     return xcd * per + (xcd < rem ? xcd : rem) + loc;
-}
-
-// Position of key `key` (within a tile) in the V^T LDS rows: bits 2 and 3 of
-// the index are swapped inside each group of 16 keys, so that the 8 keys a
-// lane contributes to one PV k-step are contiguous.
-__device__ __forceinline__ int vpos(int key) {
-    return (key & ~15) | (key & 3) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
 // Two floats to a packed bf16 pair (round to nearest even): one v_cvt_pk_bf16_f32.
@@ -155,8 +173,8 @@ __device__ __forceinline__ float halves_sum(float x) {
 template <int D, int QB, int KS, int KW, bool PATCH>
 __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     using C = Cfg<D, QB, KS, KW>;
-    constexpr int NT = C::THREADS, BN = C::BN;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[C::LDS_ELEMS];
+    constexpr int NT = C::THREADS, BN = C::BN, NST = C::NSTAGE;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -167,46 +185,47 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const int qt = logical % a.q_tiles;
     const int bh = logical / a.q_tiles;
     const int hh = bh % a.H, b = bh / a.H;
-    const uint32_t rowb = (uint32_t)a.H * D * 2;  // bytes between consecutive rows
+    const uint32_t rowb = (uint32_t)a.H * D * 2;  // bytes between consecutive rows in memory
     const uint32_t headb = (uint32_t)hh * D * 2;  // byte offset of this head in a row
-    const bool writeback = PATCH && qt == 0;
 
-    // Row 0 of this (batch, head) in each source; per-thread offsets are
-    // then row * rowb + 16-byte column, and each tile gets its own buffer
-    // resource (scalar work only) whose range ends at the source's last row,
-    // so rows past the end read as zero and writes to them are dropped.
+    // Row 0 of this (batch, head) in each source.  Each tile gets its own
+    // buffer resource (scalar work only) whose range ends at the source's
+    // last row, so rows past the end read as zero.
     const int64_t headoff = (int64_t)hh * D;
     const uint16_t* kbase = a.k + (int64_t)b * a.Nk * a.H * D + headoff;
     const uint16_t* vbase = a.v + (int64_t)b * a.Nk * a.H * D + headoff;
     const uint16_t* fkbase = PATCH ? a.fk + (int64_t)b * a.len * a.H * D + headoff : nullptr;
     const uint16_t* fvbase = PATCH ? a.fv + (int64_t)b * a.len * a.H * D + headoff : nullptr;
-    // resource over rows [row0, rows) of a source starting at `base`
     auto rows_rsrc = [&](const uint16_t* base, int row0, int rows) -> Rsrc {
         return rsrc(base + (int64_t)row0 * a.H * D, (uint32_t)(rows - row0) * rowb - headb);
     };
 
-    // LDS: two K stages then two V^T stages.  K tile t lives in K stage t%2
-    // and V tile t in V stage t%2; K runs one tile ahead of V (see the loop).
-    auto kstage = [&](int s) -> uint16_t* { return lds + s * C::K_ELEMS; };
-    auto vstage = [&](int s) -> uint16_t* { return lds + 2 * C::K_ELEMS + s * C::V_ELEMS; };
+    auto stage = [&](int s) -> unsigned char* { return lds + s * C::STAGE_BYTES; };
 
-    // Padding of every stage, written once (tile stores never touch it):
-    // K columns [D, DK) are zero; V^T rows [D, DV) are zero except row D,
-    // which holds ones when the row sums are taken on the matrix cores.
-    if constexpr (C::DK > D) {
-        for (int e = tid; e < 2 * BN; e += NT) {
-            const int st = e / BN, r = e % BN;
-            *(u32x4*)(kstage(st) + r * C::KP + D) = u32x4{0, 0, 0, 0};
-        }
+    // Constant chunks of every stage: 16 zero bytes, then bf16 {1, 0, 0, 0,
+    // 0, 0, 0, 0} (the ones entry of the row-sum row of V^T).
+    if (tid < 2 * NST) {
+        const int s = tid >> 1;
+        *(u32x4*)(stage(s) + C::CONST_OFF + 16 * (tid & 1)) =
+            (tid & 1) ? u32x4{0x3f80u, 0, 0, 0} : u32x4{0, 0, 0, 0};
     }
-    if constexpr (C::DV > D) {
-        constexpr int PR = C::DV - D, CPR = BN / 8;
-        for (int e = tid; e < 2 * PR * CPR; e += NT) {
-            const int st = e / (PR * CPR), rem = e % (PR * CPR);
-            const int r = D + rem / CPR, cc = rem % CPR;
-            const uint32_t fill = r == D ? 0x3f803f80u : 0u;  // bf16 1.0 pairs
-            *(u32x4*)(vstage(st) + r * C::VP + 8 * cc) = u32x4{fill, fill, fill, fill};
+
+    // Patch mode: this workgroup's share of the fresh slice goes into the
+    // buffer (all query tiles of a (batch, head) split the rows).  Nobody
+    // reads the slice rows of the buffer: they are taken from the fresh rows.
+    if constexpr (PATCH) {
+        const int r0 = (int)((int64_t)a.len * qt / a.q_tiles);
+        const int r1 = (int)((int64_t)a.len * (qt + 1) / a.q_tiles);
+        const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
+        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), a.off, a.Nk);
+        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), a.off, a.Nk);
+        for (int e = tid; e < (r1 - r0) * C::CH; e += NT) {
+            const int r = r0 + e / C::CH;
+            const uint32_t o = (uint32_t)r * rowb + 16 * (e % C::CH);
+            bstore(wk, o, bload(fk, o));
+            bstore(wv, o, bload(fv, o));
         }
+        wait_vmem<0>();
     }
 
     // The block's 32 query rows, as B operands (lane: query c, dims 16kk+8hf..+7).
@@ -221,39 +240,26 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
         qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
     }
+    // Make sure the query registers are complete before any tile load, so the
+    // loop body never waits on memory operations other than the tile loads.
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
 
-    // Per-thread chunks it stages, independent of the tile: K chunk i is row
-    // krow[i], 16-byte column kcol[i]; V block i is rows 4*vrg[i]..+3, column
-    // vcc[i].  koff / voff are the byte offsets from the tile's first row; a
-    // thread without a chunk gets kOOB, which no resource range reaches (row
-    // offsets stay below 2^31, checked by the host).
-    int krow[C::K_LOADS];
-    uint32_t kcol[C::K_LOADS], koff[C::K_LOADS];
+    // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
+    // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
+    // row p / CH, logical chunk (p % CH) ^ swizzle(row).  dma_row / dma_off
+    // are that row and its byte offset from the tile's first row.
+    int dma_row[C::DMA_PER_WAVE];
+    uint32_t dma_off[C::DMA_PER_WAVE];
 #pragma unroll
-    for (int i = 0; i < C::K_LOADS; ++i) {
-        const int e = tid + i * NT;
-        const bool ok = e < C::K_CHUNKS;
-        krow[i] = ok ? e / C::CH : 0;
-        kcol[i] = 16 * (e % C::CH);
-        koff[i] = ok ? (uint32_t)krow[i] * rowb + kcol[i] : kOOB;
-    }
-    // V blocks go row-group fastest across lanes: the transposed LDS writes
-    // of a block land 8 rows apart per 16-byte column, so lanes that differed
-    // in column would all hit the same banks.
-    constexpr int RG = BN / 4;  // row groups per tile
-    int vrg[C::V_LOADS], vcc[C::V_LOADS];
-    uint32_t voff[C::V_LOADS];
-#pragma unroll
-    for (int i = 0; i < C::V_LOADS; ++i) {
-        const int e = tid + i * NT;
-        const bool ok = e < C::V_BLOCKS;
-        vrg[i] = ok ? e % RG : 0;
-        vcc[i] = ok ? e / RG : 0;
-        voff[i] = ok ? (uint32_t)(4 * vrg[i]) * rowb + 16 * vcc[i] : kOOB;
+    for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
+        const int p = 64 * (wave + n * C::NW) + lane;
+        const int r = p / C::CH, pc = p % C::CH;
+        dma_row[n] = r;
+        dma_off[n] = (uint32_t)r * rowb + 16 * (pc ^ (r & C::SWZ_MASK));
     }
 
     auto in_slice = [&](int j) -> bool { return (unsigned)(j - a.off) < (unsigned)a.len; };
-
     // Where a tile's rows come from (uniform across the workgroup): all from
     // the buffer (or the chunk), all from the fresh rows, or both.
     enum { kBuf = 0, kFresh = 1, kMixed = 2 };
@@ -265,151 +271,71 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         return kMixed;
     };
 
-    u32x4 kreg[C::K_LOADS], vreg[4 * C::V_LOADS];
-
-    // Global -> registers for K tile t.  A whole-tile source needs no
-    // per-lane selects; a tile straddling a slice boundary (at most two per
-    // sweep) reads each row from its own source, the other read returning
-    // zero, and waits for its loads at once.
-    auto load_k = [&](int t) {
+    // Issue the loads of K and V tile t into stage s.
+    auto load_tile = [&](int t, int s) {
         const int kind = tile_kind(t), lo = t * BN;
+        unsigned char* kdst = stage(s);
+        unsigned char* vdst = stage(s) + C::TILE_BYTES;
         if (kind != kMixed) {
-            const Rsrc r = kind == kBuf ? rows_rsrc(kbase, lo, a.Nk) : rows_rsrc(fkbase, lo - a.off, a.len);
+            const Rsrc rk = kind == kBuf ? rows_rsrc(kbase, lo, a.Nk) : rows_rsrc(fkbase, lo - a.off, a.len);
+            const Rsrc rv = kind == kBuf ? rows_rsrc(vbase, lo, a.Nk) : rows_rsrc(fvbase, lo - a.off, a.len);
 #pragma unroll
-            for (int i = 0; i < C::K_LOADS; ++i) kreg[i] = bload(r, koff[i]);
+            for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
+                const int ins = wave + n * C::NW;
+                if (C::DMA_PER_TILE % C::NW == 0 || ins < C::DMA_PER_TILE) {
+                    dma16(rk, kdst + 1024 * ins, dma_off[n]);
+                    dma16(rv, vdst + 1024 * ins, dma_off[n]);
+                }
+            }
         } else {
-            const Rsrc rb = rows_rsrc(kbase, lo, a.Nk), rf = rows_rsrc(fkbase, 0, a.len);
+            // the tile straddles a slice boundary (at most two per sweep):
+            // each lane loads its row from its own source
+            const Rsrc rk = rows_rsrc(kbase, lo, a.Nk), rv = rows_rsrc(vbase, lo, a.Nk);
+            const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
+            const uint32_t shift = (uint32_t)(lo - a.off) * rowb;  // fresh row = tile row + lo - off
 #pragma unroll
-            for (int i = 0; i < C::K_LOADS; ++i) {
-                const int j = lo + krow[i];
-                const bool f = in_slice(j) && koff[i] != kOOB;
-                kreg[i] = bload(rb, f ? kOOB : koff[i]) |
-                          bload(rf, f ? (uint32_t)(j - a.off) * rowb + kcol[i] : kOOB);
-            }
-        }
-    };
-    auto load_v = [&](int t) {
-        const int kind = tile_kind(t), lo = t * BN;
-        if (kind != kMixed) {
-            const Rsrc r = kind == kBuf ? rows_rsrc(vbase, lo, a.Nk) : rows_rsrc(fvbase, lo - a.off, a.len);
-#pragma unroll
-            for (int i = 0; i < C::V_LOADS; ++i)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) vreg[4 * i + q] = bload(r, voff[i] == kOOB ? kOOB : voff[i] + q * rowb);
-        } else {
-            const Rsrc rb = rows_rsrc(vbase, lo, a.Nk), rf = rows_rsrc(fvbase, 0, a.len);
-#pragma unroll
-            for (int i = 0; i < C::V_LOADS; ++i)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int j = lo + 4 * vrg[i] + q;
-                    const bool f = in_slice(j) && voff[i] != kOOB;
-                    const uint32_t o = voff[i] == kOOB ? kOOB : voff[i] + q * rowb;
-                    vreg[4 * i + q] = bload(rb, f ? kOOB : o) |
-                                      bload(rf, f ? (uint32_t)(j - a.off) * rowb + 16 * vcc[i] : kOOB);
-                }
-        }
-    };
-
-    // Registers -> LDS stage, plus (patch mode, first query tile only) the
-    // fresh rows into the buffer.
-    auto store_k = [&](int st, int t) {
-        uint16_t* Ks = kstage(st);
-#pragma unroll
-        for (int i = 0; i < C::K_LOADS; ++i) {
-            const int e = tid + i * NT;
-            if (C::K_CHUNKS % NT == 0 || e < C::K_CHUNKS)
-                *(u32x4*)(Ks + krow[i] * C::KP + kcol[i] / 2) = kreg[i];
-        }
-        if constexpr (PATCH) {
-            const int kind = tile_kind(t), lo = t * BN;
-            if (writeback && kind != kBuf) {
-                const Rsrc rw = rows_rsrc(a.wk + (kbase - a.k), lo, a.Nk);
-#pragma unroll
-                for (int i = 0; i < C::K_LOADS; ++i) {
-                    const bool f = kind == kFresh || in_slice(lo + krow[i]);
-                    bstore(rw, f ? koff[i] : kOOB, kreg[i]);
-                }
-            }
-        }
-    };
-    auto store_v = [&](int st, int t) {
-        uint16_t* Vt = vstage(st);
-#pragma unroll
-        for (int i = 0; i < C::V_LOADS; ++i) {
-            const int e = tid + i * NT;
-            if (C::V_BLOCKS % NT == 0 || e < C::V_BLOCKS) {
-                const int cc = vcc[i];
-                const u32x4 r0 = vreg[4 * i], r1 = vreg[4 * i + 1];
-                const u32x4 r2 = vreg[4 * i + 2], r3 = vreg[4 * i + 3];
-                const int pos = vpos(4 * vrg[i]);
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    // dims 8cc+2w (low halves) and 8cc+2w+1 (high halves) of the 4 rows
-                    const u32x2 even = {(r0[w] & 0xffffu) | (r1[w] << 16),
-                                        (r2[w] & 0xffffu) | (r3[w] << 16)};
-                    const u32x2 odd = {(r0[w] >> 16) | (r1[w] & 0xffff0000u),
-                                       (r2[w] >> 16) | (r3[w] & 0xffff0000u)};
-                    *(u32x2*)(Vt + (8 * cc + 2 * w) * C::VP + pos) = even;
-                    *(u32x2*)(Vt + (8 * cc + 2 * w + 1) * C::VP + pos) = odd;
-                }
-            }
-        }
-        if constexpr (PATCH) {
-            const int kind = tile_kind(t), lo = t * BN;
-            if (writeback && kind != kBuf) {
-                const Rsrc rw = rows_rsrc(a.wv + (vbase - a.v), lo, a.Nk);
-#pragma unroll
-                for (int i = 0; i < C::V_LOADS; ++i)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const bool f = kind == kFresh || in_slice(lo + 4 * vrg[i] + q);
-                        const uint32_t o = voff[i] == kOOB ? kOOB : voff[i] + q * rowb;
-                        bstore(rw, f ? o : kOOB, vreg[4 * i + q]);
+            for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
+                const int ins = wave + n * C::NW;
+                if (C::DMA_PER_TILE % C::NW == 0 || ins < C::DMA_PER_TILE) {
+                    if (in_slice(lo + dma_row[n])) {
+                        dma16(fk, kdst + 1024 * ins, dma_off[n] + shift);
+                        dma16(fv, vdst + 1024 * ins, dma_off[n] + shift);
+                    } else {
+                        dma16(rk, kdst + 1024 * ins, dma_off[n]);
+                        dma16(rv, vdst + 1024 * ins, dma_off[n]);
                     }
-            }
-        }
-    };
-
-    const int kw0 = kh * KW;  // this wave's first key within a tile
-
-    // S^T for this wave's KW keys of K tile in stage st x its 32 queries:
-    // S[kb][i] = score of key kw0 + 32kb + 8(i/4) + 4hf + (i%4) against query c.
-    auto qk = [&](int st, f32x16 (&S)[C::NKB]) {
-        const uint16_t* Ks = kstage(st);
-#pragma unroll
-        for (int kb = 0; kb < C::NKB; ++kb) S[kb] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < C::KSTEPS; ++kk)
-#pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb) {
-                const bf16x8 ka = *(const bf16x8*)(Ks + (kw0 + 32 * kb + c) * C::KP + 16 * kk + 8 * hf);
-                S[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], S[kb], 0, 0, 0);
-            }
-    };
-    // Keys of tile t past the end get -inf; the row max of the rest.
-    auto mask_max = [&](int t, f32x16 (&S)[C::NKB]) -> float {
-        if ((t + 1) * BN > a.Nk) {
-#pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = t * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
-                    if (key >= a.Nk) S[kb][i] = -INFINITY;
                 }
+            }
         }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < C::NKB; ++kb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[kb][i]);
-        return halves_max(mx);
     };
 
-    // Make sure the query registers are complete before the loop, so the
-    // loop body never waits on memory operations other than the staged tiles.
+    // LDS byte offsets (within a stage) of this lane's operand reads.
+    //  K (A operand of S^T): row kw0 + 32kb + c, logical chunk 2kk + hf;
+    //  chunks past d read the zero chunk.
+    //  V (A operand of O^T, transposed read from the V tile, which follows
+    //  the K tile in the stage): in each 16-lane group, lane
+    //  4j+q reads dims d0+4q..+3 of key kw0 + 16ks + 8e + 4hf + j, where
+    //  d0 = 32db + 16*(group & 1) and e = 0, 1 selects the half k-step;
+    //  lane i of the group then holds dim d0 + i of the four keys.  Padding
+    //  dims read the constant chunks (ones for dim d, zeros after it).
+    const int kw0 = kh * KW;  // this wave's first key within a tile
+    uint32_t kaddr[C::KSTEPS];
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
+    for (int kk = 0; kk < C::KSTEPS; ++kk) {
+        const int r = kw0 + c, lc = 2 * kk + hf;
+        kaddr[kk] = lc < C::CH ? r * C::ROWB + 16 * (lc ^ (r & C::SWZ_MASK)) : C::CONST_OFF;
+    }
+    const int gi = lane & 15, grp = lane >> 4;
+    const int vkey0 = kw0 + 4 * hf + (gi >> 2);
+    uint32_t vaddr[C::DBLK];
+#pragma unroll
+    for (int db = 0; db < C::DBLK; ++db) {
+        const int dim = 32 * db + 16 * (grp & 1) + 4 * (gi & 3);
+        if (dim < D)
+            vaddr[db] = C::TILE_BYTES + vkey0 * C::ROWB + 16 * ((dim >> 3) ^ (vkey0 & C::SWZ_MASK)) + 2 * (dim & 7);
+        else
+            vaddr[db] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
+    }
 
     f32x16 oacc[C::DBLK];
 #pragma unroll
@@ -418,36 +344,60 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     float l_run = 0.f;        // this lane's share of the running sum (VALU-summed case)
     const float thr = kRescaleLog2 / a.c2;
 
-    // Software pipeline over tiles.  Iteration t computes the weights of tile
-    // t while the scores of tile t+1 run on the matrix cores, then P(t) V(t)
-    // while the row max of tile t+1 and the staging of K(t+2), V(t+1) run on
-    // the vector units.  So K tile t+1 and V tile t are read during iteration
-    // t, and K(t+2) / V(t+1) are written into the stages that K(t) / V(t-1)
-    // left free at the previous barrier: two stages each, one barrier per tile.
+    __syncthreads();  // the constant chunks are written
+
     const int ntiles = (a.Nk + BN - 1) / BN;
-    f32x16 SA[C::NKB], SB[C::NKB];
-    float mx = -INFINITY;
-    if (ntiles > 0) {
-        load_k(0);
-        load_v(0);
-        store_k(0, 0);
-        store_v(0, 0);
-        if (ntiles > 1) {
-            load_k(1);
-            store_k(1, 1);
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t)
+        if (t < ntiles) load_tile(t, t);
+
+    for (int t = 0; t < ntiles; ++t) {
+        // Tile t must have landed (up to NST-2 younger tiles may still be in
+        // flight) before anyone reads it: each wave waits for its own loads,
+        // then all meet.  A bare s_barrier: the full __syncthreads fence would
+        // also drain the younger loads.  Reads of the stage being refilled
+        // below finished in the previous iteration (their results were
+        // consumed there), so no LDS wait is needed either.
+        const int younger = min(ntiles - 1 - t, NST - 2);
+        if (younger >= 1) wait_vmem<C::DMA_MIN_PER_WAVE>();
+        else wait_vmem<0>();
+        __builtin_amdgcn_s_barrier();
+        // everybody is past tile t-1, so its stage takes tile t+NST-1
+        if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
+
+        const unsigned char* st = stage(t % NST);
+
+        // S^T for this wave's KW keys x 32 queries: sacc[kb][i] = score of
+        // key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against query c.
+        f32x16 sacc[C::NKB];
+#pragma unroll
+        for (int kb = 0; kb < C::NKB; ++kb) sacc[kb] = f32x16{};
+#pragma unroll
+        for (int kk = 0; kk < C::KSTEPS; ++kk)
+#pragma unroll
+            for (int kb = 0; kb < C::NKB; ++kb) {
+                uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
+                if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
+                const bf16x8 ka = *(const bf16x8*)(st + ad);
+                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], sacc[kb], 0, 0, 0);
+            }
+
+        if ((t + 1) * BN > a.Nk) {  // ragged last tile: keys past the end get -inf
+#pragma unroll
+            for (int kb = 0; kb < C::NKB; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int key = t * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
+                    if (key >= a.Nk) sacc[kb][i] = -INFINITY;
+                }
         }
-    }
-    __syncthreads();
-    if (ntiles > 0) {
-        qk(0, SA);
-        mx = mask_max(0, SA);
-    }
-    __syncthreads();  // K stage 0 is rewritten in iteration 0
 
-    auto step = [&](int t, f32x16 (&S)[C::NKB], f32x16 (&Sn)[C::NKB]) {
-        if (t + 2 < ntiles) load_k(t + 2);
-        if (t + 1 < ntiles) load_v(t + 1);
-
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < C::NKB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
+        mx = halves_max(mx);
         if (__builtin_amdgcn_ballot_w64(mx > m_ref + thr) != 0) {
             const float m_new = fmaxf(m_ref, mx);
             // m_new = -inf only while a wave has seen no valid key: keep alpha finite
@@ -460,48 +410,35 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         // with no valid key yet every score is -inf and any finite shift gives 0
         const float mc = m_ref == -INFINITY ? 0.f : m_ref * a.c2;
 
-        // scores of tile t+1 (a tile past the end computes garbage that is
-        // never used) || weights of tile t, packed as PV B operands
-        qk((t + 1) & 1, Sn);
-        bf16x8 pb[C::NKS];
+        // O^T += V^T P^T over KW/16 k-steps of 16 keys.
 #pragma unroll
         for (int ks = 0; ks < C::NKS; ++ks) {
             const int kb = ks >> 1, i0 = 8 * (ks & 1);
             float p[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[kb][i0 + e], a.c2, -mc));
+                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i0 + e], a.c2, -mc));
                 if constexpr (!C::SUM_BY_MFMA) l_run += p[e];
             }
             u32x4 pw;
 #pragma unroll
             for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
-            pb[ks] = __builtin_bit_cast(bf16x8, pw);
-        }
-
-        // O^T += V^T P^T over KW/16 k-steps of 16 keys || row max of tile t+1
-        const uint16_t* Vt = vstage(t & 1);
-#pragma unroll
-        for (int ks = 0; ks < C::NKS; ++ks)
+            const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
-                const bf16x8 va = *(const bf16x8*)(Vt + (32 * db + c) * C::VP + kw0 + 16 * ks + 8 * hf);
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[ks], oacc[db], 0, 0, 0);
+                uint32_t a0 = vaddr[db] + 16 * ks * C::ROWB, a1 = a0 + 8 * C::ROWB;
+                if (32 * db + 31 >= D && vaddr[db] >= (uint32_t)C::CONST_OFF) a0 = a1 = vaddr[db];
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st + a0));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st + a1));
+                const s16x8 v8 = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[db], 0, 0, 0);
             }
-        mx = mask_max(t + 1, Sn);
-
-        if (t + 2 < ntiles) store_k(t & 1, t + 2);
-        if (t + 1 < ntiles) store_v((t + 1) & 1, t + 1);
-        __syncthreads();
-    };
-    for (int t = 0; t < ntiles; t += 2) {
-        step(t, SA, SB);
-        if (t + 1 < ntiles) step(t + 1, SB, SA);
+        }
     }
+    __syncthreads();  // every wave is done with the stages
 
-    // Merge the KS partial sweeps of each query block (the K/V stages are no
-    // longer read: the loop ended with a barrier).  Slots are lane-major so
-    // the exchange is free of bank conflicts.
+    // Merge the KS partial sweeps of each query block.  Slots are lane-major
+    // so the exchange is free of bank conflicts.
     if constexpr (KS > 1) {
         float* xs = (float*)lds;
         if (kh > 0) {
@@ -596,8 +533,8 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Two shapes of 8-wave workgroup: 128 query rows x 2 key splits of 64 keys,
-// or 64 query rows x 4 key splits of 32 keys for query counts whose 128-row
+// Two shapes of 8-wave workgroup: 128 query rows x 2 key splits ("wide"),
+// or 64 query rows x 4 key splits ("narrow") for query counts whose 128-row
 // tiles would leave many of the 256 CUs idle.
 constexpr int kCUs = 256;
 
@@ -618,17 +555,17 @@ int forced_shape() {
 
 template <int D, bool PATCH>
 hipError_t dispatch(const AttnParams& p, hipStream_t s) {
+    // keys per wave per tile: 64 at d <= 72, 32 at d = 128 (register budget)
+    constexpr int KWW = D > 96 ? 32 : 64;
     const int forced = forced_shape();
-    if (forced == 1) return launch<D, 4, 2, 64, PATCH>(p, s);
+    if (forced == 1) return launch<D, 4, 2, KWW, PATCH>(p, s);
     if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
-    // at d = 128 the wide shape's two score tiles do not fit in registers
-    if constexpr (D > 96) return launch<D, 2, 4, 32, PATCH>(p, s);
     const int64_t bh = (int64_t)p.B * p.H;
     const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
     const double qfill_w = (double)p.Nq / ((p.Nq + 127) / 128 * 128.0);
     const double qfill_n = (double)p.Nq / ((p.Nq + 63) / 64 * 64.0);
     if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, PATCH>(p, s);
-    return launch<D, 4, 2, 64, PATCH>(p, s);
+    return launch<D, 4, 2, KWW, PATCH>(p, s);
 }
 
 }  // namespace
