@@ -53,6 +53,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <type_traits>
+
 namespace xdit {
 namespace {
 
@@ -146,6 +148,43 @@ __device__ __forceinline__ void wait_vmem() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// Transposing LDS read (ds_read_b64_tr_b16) at byte address a + OFF, issued
+// without a wait: the caller waits with lds_wait() before using the result.
+// Written as inline assembly so that the compiler does not also drain the
+// in-flight tile loads before it (it cannot tell that they target other LDS
+// bytes).
+template <int OFF>
+__device__ __forceinline__ u32x2 tr_read(uint32_t a) {
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    u32x2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+    return r;
+}
+// Wait for all LDS reads of this wave; the operands are the registers those
+// reads fill, so nothing reads them before the wait.
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x2 (&r)[N][2]) {
+    static_assert(N >= 1 && N <= 4, "up to four operand blocks");
+    if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]));
+    if constexpr (N == 2)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]));
+    if constexpr (N == 3)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]),
+                     "+v"(r[2][0]), "+v"(r[2][1]));
+    if constexpr (N == 4)
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]),
+                     "+v"(r[2][0]), "+v"(r[2][1]), "+v"(r[3][0]), "+v"(r[3][1]));
+}
+
 __device__ __forceinline__ int xcd_remap(int pid, int total) {
     const int per = total >> 3, rem = total & 7;
     const int xcd = pid & 7, loc = pid >> 3;
@@ -201,6 +240,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     };
 
     auto stage = [&](int s) -> unsigned char* { return lds + s * C::STAGE_BYTES; };
+    const uint32_t lds_u32 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)lds;
 
     // Constant chunks of every stage: 16 zero bytes, then bf16 {1, 0, 0, 0,
     // 0, 0, 0, 0} (the ones entry of the row-sum row of V^T).
@@ -361,7 +401,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         const int younger = min(ntiles - 1 - t, NST - 2);
         if (younger >= 1) wait_vmem<C::DMA_MIN_PER_WAVE>();
         else wait_vmem<0>();
+        asm volatile("" ::: "memory");  // no LDS access moves across the barrier
         __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
         // everybody is past tile t-1, so its stage takes tile t+NST-1
         if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
 
@@ -410,10 +452,28 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         // with no valid key yet every score is -inf and any finite shift gives 0
         const float mc = m_ref == -INFINITY ? 0.f : m_ref * a.c2;
 
-        // O^T += V^T P^T over KW/16 k-steps of 16 keys.
-#pragma unroll
-        for (int ks = 0; ks < C::NKS; ++ks) {
-            const int kb = ks >> 1, i0 = 8 * (ks & 1);
+        // O^T += V^T P^T over KW/16 k-steps of 16 keys.  Each step issues its
+        // V^T reads, computes its weights while they are in flight, waits,
+        // then runs the MFMAs.
+        const uint32_t vst = lds_u32 + (uint32_t)((t % NST) * C::STAGE_BYTES);
+        static_for<0, C::NKS>([&](auto ksc) {
+            constexpr int ks = decltype(ksc)::value;
+            u32x2 vr[C::DBLK][2];
+            static_for<0, C::DBLK>([&](auto dbc) {
+                constexpr int db = decltype(dbc)::value;
+                if constexpr (32 * db + 31 >= D && C::DV > D) {
+                    // block with padding dims: their lanes keep reading the constant chunk
+                    const bool cst = vaddr[db] >= (uint32_t)C::CONST_OFF;
+                    const uint32_t a0 = vst + vaddr[db] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
+                    const uint32_t a1 = vst + vaddr[db] + (cst ? 0u : (uint32_t)((16 * ks + 8) * C::ROWB));
+                    vr[db][0] = tr_read<0>(a0);
+                    vr[db][1] = tr_read<0>(a1);
+                } else {
+                    vr[db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db]);
+                    vr[db][1] = tr_read<(16 * ks + 8) * C::ROWB>(vst + vaddr[db]);
+                }
+            });
+            constexpr int kb = ks >> 1, i0 = 8 * (ks & 1);
             float p[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -424,16 +484,14 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
             for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
             const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+            lds_wait(vr);
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
-                uint32_t a0 = vaddr[db] + 16 * ks * C::ROWB, a1 = a0 + 8 * C::ROWB;
-                if (32 * db + 31 >= D && vaddr[db] >= (uint32_t)C::CONST_OFF) a0 = a1 = vaddr[db];
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st + a0));
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st + a1));
-                const s16x8 v8 = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[db], 0, 0, 0);
+                const u32x4 v4 = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb, oacc[db],
+                                                                   0, 0, 0);
             }
-        }
+        });
     }
     __syncthreads();  // every wave is done with the stages
 
