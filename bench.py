@@ -9,9 +9,11 @@ workload (default: Pixart 1024px, B=2 H=16 d=72, 4096 tokens):
   * the sequence-parallel share: chunk attention of the local query shard over
     each K/V chunk (O and LSE), then the LSE merge of the partials.
 Inputs are synthetic (seeded N(0,1); stale K/V = fresh + N(0, 0.05^2)) and
-resident in HBM before timing starts.  W untimed steps, then K timed steps
-between synchronisations; HIP events around every call give each kernel's
-average duration.  Prints ONE JSON line.
+resident in HBM before timing starts.  W untimed steps (the default lets the
+GPU clocks settle), then K timed steps between synchronisations with events
+only at the ends; then K more steps with HIP events around each run of
+consecutive launches of one kernel give each kernel's average duration.
+Prints ONE JSON line.
 
 `value` is algorithmic attention FLOP/s (4*B*H*Nq*Nk*d per call) over the
 whole step.  `roofline` refers to the kernel with the largest share of the
@@ -33,17 +35,33 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
-# HBM traffic per launch of the dominant kernel, from rocprofv3 --pmc
-# FETCH_SIZE / WRITE_SIZE, scaled by the copy-kernel calibration factor.
-# None until counters for the current kernel build are taken.
-MEASURED_TRAFFIC = {}
+# HBM traffic per launch of the dominant kernel, in bytes: rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE (KiB per dispatch, one counter per run), scaled by
+# what the same counters read for kv_update_kernel copying a known size
+# (FETCH x 1.9944, WRITE x 1.0).  Each entry holds the sha256 prefix of the
+# kernel source it was taken on; a different source reports null.
+MEASURED_TRAFFIC = {
+    ("pixart", "patch_attn"): {"bytes": (51935 + 13826) * 1024, "src": "a211186b2a998c9c"},
+}
+
+
+def traffic_of(workload: str, kind: str):
+    import hashlib
+
+    e = MEASURED_TRAFFIC.get((workload, kind))
+    if e is None:
+        return None
+    src = os.path.join(ROOT, "paper_2411_01738_amd", "csrc", "attn_bf16.hip")
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    return e["bytes"] if sha == e["src"] else None
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="pixart",
                     choices=["tiny", "pixart", "sd3", "flux", "cog"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -80,24 +98,37 @@ def cpu_baseline(w, t, target_s: float):
             jobs.append((f"chunk {r}", q1 - q0, e - s,
                          lambda rows, k=k, v=v: orc.attention(q, k, v, rows=rows)))
 
-    # calibrate on a few rows of the first call
+    # calibrate the cost of one (query row x key) on a few rows of the first
+    # call; the first probe also starts the oracle's thread pool
     desc0, nq0, nk0, run0 = jobs[0]
     probe = np.linspace(0, nq0 - 1, min(64, nq0)).astype(np.int64)
+    run0(probe)
     t0 = time.perf_counter()
     run0(probe)
-    per_row = (time.perf_counter() - t0) / len(probe)
+    per_unit = (time.perf_counter() - t0) / (len(probe) * nk0)
+    # whole calls in step order, the step repeated if it is short, the last
+    # call cut to an evenly spaced subset of its rows to stay near target_s
     flops, spent, parts = 0.0, 0.0, []
-    for desc, nq, nk, run in jobs:
-        left = target_s - spent
-        if left <= 0.2 * target_s and parts:
-            break
-        n = nq if per_row * nq <= left else max(1, int(left / per_row))
-        rows = np.arange(nq, dtype=np.int64) if n >= nq else np.linspace(0, nq - 1, n).astype(np.int64)
-        t0 = time.perf_counter()
-        run(rows)
-        spent += time.perf_counter() - t0
-        flops += w.attn_flops(len(rows), nk)
-        parts.append(f"{desc} ({len(rows)}/{nq} rows)")
+    for rep in range(1000):
+        for desc, nq, nk, run in jobs:
+            left = target_s - spent
+            if left <= 0.05 * target_s:
+                break
+            n = min(nq, max(1, int(left / (per_unit * nk))))
+            rows = (np.arange(nq, dtype=np.int64) if n >= nq
+                    else np.linspace(0, nq - 1, n).astype(np.int64))
+            t0 = time.perf_counter()
+            run(rows)
+            dt = time.perf_counter() - t0
+            spent += dt
+            per_unit = dt / (len(rows) * nk)
+            flops += w.attn_flops(len(rows), nk)
+            parts.append(f"{desc} ({len(rows)}/{nq} rows)")
+        else:
+            continue
+        break
+    if len(parts) > 6:
+        parts = parts[:3] + [f"... {len(parts) - 6} more calls ..."] + parts[-3:]
     return {
         "value": flops / spent / 1e12,
         "unit": "TFLOP/s",
@@ -144,29 +175,47 @@ def main():
         hp.step()
     torch.cuda.synchronize()
 
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in calls] for _ in range(args.steps)]
+    # timed region: exactly K steps, events only at its two ends
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for s in range(args.steps):
-        for i, (_, fn, _, _) in enumerate(calls):
-            ev[s][i][0].record(stream)
+    for _ in range(args.steps):
+        for _, fn, _, _ in calls:
             fn()
-            ev[s][i][1].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_per_step = total_ms / args.steps
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    # per-kernel durations: K more steps with HIP events on the launch stream
+    # around each run of consecutive launches of one kernel (the M patch
+    # steps, the chunk steps, the merge); an event pair costs the stream a few
+    # microseconds, so it is kept out of the timed region above
+    groups = []  # (kind, first call, end call)
+    for i, (kind, _, _, _) in enumerate(calls):
+        if groups and groups[-1][0] == kind:
+            groups[-1][2] = i + 1
+        else:
+            groups.append([kind, i, i + 1])
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in groups] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        for g, (_, a, b) in enumerate(groups):
+            ev[s][g][0].record(stream)
+            for _, fn, _, _ in calls[a:b]:
+                fn()
+            ev[s][g][1].record(stream)
+    torch.cuda.synchronize()
 
     kinds = {}
-    for i, (kind, _, flops, nbytes) in enumerate(calls):
+    for g, (kind, a, b) in enumerate(groups):
         d = kinds.setdefault(kind, {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
         for s in range(args.steps):
-            d["ms"] += ev[s][i][0].elapsed_time(ev[s][i][1])
-        d["launches"] += args.steps
-        d["flops"] += flops * args.steps
-        d["bytes"] += nbytes * args.steps
+            d["ms"] += ev[s][g][0].elapsed_time(ev[s][g][1])
+        d["launches"] += (b - a) * args.steps
+        for _, _, flops, nbytes in calls[a:b]:
+            d["flops"] += flops * args.steps
+            d["bytes"] += nbytes * args.steps
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kern = {}
     for kind, d in kinds.items():
@@ -180,23 +229,72 @@ def main():
             e.update(gbs=round(gbs, 1), frac_hbm=round(gbs / PEAK_HBM_GBS, 4))
         kern[kind] = e
 
-    # stand-alone K/V-slice update (the patch kernel does it fused): its GB/s
+    # stand-alone K/V-slice update (the patch kernel does it fused): its GB/s.
+    # Warm: back-to-back launches through the C ABI with the arguments
+    # marshalled once (a launch takes less time than the binding's checks).
+    # Cold: each launch after a 1 GiB write that evicts L2 and the MALL,
+    # bracketed by its own events (which add about a microsecond).
     if w.patches():
-        from paper_2411_01738_amd import xdit_kv_update
-
-        reps = 20
         off, ln = w.patches()[0]
+        L = _lib.lib()
+        L.xdit_set_stream(stream.cuda_stream)
+        upd = (hp.kv_buf.data_ptr(), off, ln, hp.patch_k[0].data_ptr(), hp.patch_v[0].data_ptr(),
+               w.B, w.N, w.H, w.d, _lib.XDIT_BF16 if w.dtype == "bf16" else _lib.XDIT_F32)
+        _lib.check(L.xdit_kv_update(*upd))
+        reps = 200
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        xdit_kv_update(hp.kv_buf, off, ln, hp.patch_k[0], hp.patch_v[0])
+        torch.cuda.synchronize()
         a.record(stream)
-        for _ in range(reps):
-            xdit_kv_update(hp.kv_buf, off, ln, hp.patch_k[0], hp.patch_v[0])
+        rcs = [L.xdit_kv_update(*upd) for _ in range(reps)]
         b.record(stream)
         torch.cuda.synchronize()
+        for rc in rcs:
+            _lib.check(rc)
+        warm_us = a.elapsed_time(b) * 1e3 / reps
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        cold = []
+        for _ in range(20):
+            flush.fill_(1.0)
+            a.record(stream)
+            _lib.check(L.xdit_kv_update(*upd))
+            b.record(stream)
+            torch.cuda.synchronize()
+            cold.append(a.elapsed_time(b) * 1e3)
+        del flush
+        cold_us = sorted(cold)[len(cold) // 2]
+        nb = hp.update_bytes(0)
+        kern["kv_update"] = {"avg_us": round(warm_us, 3), "gbs": round(nb / warm_us / 1e3, 1),
+                             "frac_hbm": round(nb / warm_us / 1e3 / PEAK_HBM_GBS, 4),
+                             "cold_median_us": round(cold_us, 3),
+                             "cold_gbs": round(nb / cold_us / 1e3, 1),
+                             "note": "outside the step: warm back-to-back, and cold after"
+                                     " evicting L2/MALL"}
+
+    # the merge is one launch per step, so its in-step events include their
+    # own overhead; back-to-back launches through the C ABI give its duration
+    if hp.sp_q is not None:
+        import ctypes
+
+        L = _lib.lib()
+        L.xdit_set_stream(stream.cuda_stream)
+        n = len(hp.chunk_out)
+        optrs = (ctypes.c_void_p * n)(*[o.data_ptr() for o in hp.chunk_out])
+        lptrs = (ctypes.c_void_p * n)(*[x.data_ptr() for x in hp.chunk_lse])
+        nq = w.sp_q[1] - w.sp_q[0]
+        mrg = (optrs, lptrs, n, hp.sp_out.data_ptr(), hp.sp_lse.data_ptr(), w.B, nq, w.H, w.d,
+               _lib.XDIT_BF16 if w.dtype == "bf16" else _lib.XDIT_F32)
+        reps = 50
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        rcs = [L.xdit_lse_merge(*mrg) for _ in range(reps)]
+        b.record(stream)
+        torch.cuda.synchronize()
+        for rc in rcs:
+            _lib.check(rc)
         us = a.elapsed_time(b) * 1e3 / reps
-        gbs = hp.update_bytes(0) / (us / 1e6) / 1e9
-        kern["kv_update"] = {"avg_us": round(us, 3), "gbs": round(gbs, 1),
-                             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "note": "warm, outside the step"}
+        kern["lse_merge"].update(back_to_back_us=round(us, 3),
+                                 back_to_back_gbs=round(hp.merge_bytes() / us / 1e3, 1))
 
     step_flops = hp.step_flops()
     value = step_flops / (ms_per_step / 1e3) / 1e12
@@ -214,7 +312,7 @@ def main():
         achieved = per_launch / avg_s / 1e9
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = MEASURED_TRAFFIC.get((w.name, dom))
+    roof["traffic"] = traffic_of(w.name, dom)
 
     cpu = None
     if args.cpu_seconds > 0:

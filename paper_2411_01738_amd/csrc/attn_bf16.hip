@@ -72,12 +72,12 @@ constexpr int kRsrcFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kRescaleLog2 = 8.0f;    // raise the reference max only beyond 2^8 growth
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
 
-template <int D, int QB_, int KS_, int KW_>
+template <int D, int QB_, int KS_, int KW_, int QP_>
 struct Cfg {
-    static constexpr int QB = QB_, KS = KS_, KW = KW_;
+    static constexpr int QB = QB_, KS = KS_, KW = KW_, QP = QP_;
     static constexpr int NW = QB * KS;               // waves per workgroup
     static constexpr int THREADS = 64 * NW;
-    static constexpr int BM = 32 * QB;               // query rows per workgroup
+    static constexpr int BM = 32 * QP * QB;          // query rows per workgroup
     static constexpr int BN = KS * KW;               // keys per tile
     static constexpr int DK = (D + 15) / 16 * 16;    // QK^T contraction length, padded to 16
     static constexpr int DV = (D + 31) / 32 * 32;    // PV output rows, padded to 32
@@ -97,9 +97,10 @@ struct Cfg {
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = DV > D;      // a padding row of V^T holds ones
-    // end-of-sweep exchange: one slot (m, l, O^T accumulators) per partial wave
+    // end-of-sweep exchange: one slot (m, l, O^T accumulators) per query
+    // block of each partial wave
     static constexpr int XSLOT = 64 * (2 + 16 * DBLK);  // floats
-    static constexpr int X_BYTES = 4 * QB * (KS - 1) * XSLOT;
+    static constexpr int X_BYTES = 4 * QB * QP * (KS - 1) * XSLOT;
     static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES > X_BYTES ? NSTAGE * STAGE_BYTES : X_BYTES;
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
     static_assert(DV - D == 0 || DV - D == 24, "V padding handled for d = 72 only");
@@ -209,16 +210,16 @@ __device__ __forceinline__ float halves_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QB, int KS, int KW, bool PATCH>
+template <int D, int QB, int KS, int KW, int QP, bool PATCH>
 __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
-    using C = Cfg<D, QB, KS, KW>;
+    using C = Cfg<D, QB, KS, KW, QP>;
     constexpr int NT = C::THREADS, BN = C::BN, NST = C::NSTAGE;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int c = lane & 31, hf = lane >> 5;
-    const int qb = wave % QB, kh = wave / QB;  // query block, key split
+    const int qb = wave % QB, kh = wave / QB;  // query-block group, key split
 
     const int logical = xcd_remap(blockIdx.x, gridDim.x);
     const int qt = logical % a.q_tiles;
@@ -268,22 +269,31 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         wait_vmem<0>();
     }
 
-    // The block's 32 query rows, as B operands (lane: query c, dims 16kk+8hf..+7).
-    const int qrow = qt * C::BM + qb * 32 + c;
-    const bool qvalid = qrow < a.Nq;
+    // The wave's QP blocks of 32 query rows, as B operands (lane: query c,
+    // dims 16kk+8hf..+7).  Each K or V^T operand read from LDS then feeds QP
+    // MFMAs.
+    int qrow[QP];
+    bool qvalid[QP];
     const Rsrc rq = rsrc(a.q + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
     const Rsrc ro = rsrc(a.out + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
-    bf16x8 qf[C::KSTEPS];
+    bf16x8 qf[QP][C::KSTEPS];
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int col = 16 * kk + 8 * hf;
-        const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
-        qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
+    for (int qp = 0; qp < QP; ++qp) {
+        qrow[qp] = qt * C::BM + (qb * QP + qp) * 32 + c;
+        qvalid[qp] = qrow[qp] < a.Nq;
+#pragma unroll
+        for (int kk = 0; kk < C::KSTEPS; ++kk) {
+            const int col = 16 * kk + 8 * hf;
+            const uint32_t o = (qvalid[qp] && col < D) ? (uint32_t)qrow[qp] * rowb + headb + 2 * col : kOOB;
+            qf[qp][kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
+        }
     }
     // Make sure the query registers are complete before any tile load, so the
     // loop body never waits on memory operations other than the tile loads.
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
+    for (int qp = 0; qp < QP; ++qp)
+#pragma unroll
+        for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[qp][kk]));
 
     // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
     // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
@@ -377,11 +387,16 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             vaddr[db] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
     }
 
-    f32x16 oacc[C::DBLK];
+    f32x16 oacc[QP][C::DBLK];
+    float m_ref[QP], l_run[QP];  // reference max of the raw dot products (this wave's
+                                 // keys); this lane's share of the running sum
 #pragma unroll
-    for (int db = 0; db < C::DBLK; ++db) oacc[db] = f32x16{};
-    float m_ref = -INFINITY;  // reference max of the raw dot products (this wave's keys)
-    float l_run = 0.f;        // this lane's share of the running sum (VALU-summed case)
+    for (int qp = 0; qp < QP; ++qp) {
+#pragma unroll
+        for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] = f32x16{};
+        m_ref[qp] = -INFINITY;
+        l_run[qp] = 0.f;
+    }
     const float thr = kRescaleLog2 / a.c2;
 
     __syncthreads();  // the constant chunks are written
@@ -409,11 +424,14 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 
         const unsigned char* st = stage(t % NST);
 
-        // S^T for this wave's KW keys x 32 queries: sacc[kb][i] = score of
-        // key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against query c.
-        f32x16 sacc[C::NKB];
+        // S^T for this wave's KW keys x 32 queries of block qp: sacc[qp][kb][i]
+        // = score of key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against
+        // query c of the block.
+        f32x16 sacc[QP][C::NKB];
 #pragma unroll
-        for (int kb = 0; kb < C::NKB; ++kb) sacc[kb] = f32x16{};
+        for (int qp = 0; qp < QP; ++qp)
+#pragma unroll
+            for (int kb = 0; kb < C::NKB; ++kb) sacc[qp][kb] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
@@ -421,7 +439,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
                 if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
                 const bf16x8 ka = *(const bf16x8*)(st + ad);
-                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], sacc[kb], 0, 0, 0);
+#pragma unroll
+                for (int qp = 0; qp < QP; ++qp)
+                    sacc[qp][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[qp][kk], sacc[qp][kb], 0, 0, 0);
             }
 
         if ((t + 1) * BN > a.Nk) {  // ragged last tile: keys past the end get -inf
@@ -430,27 +450,33 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int key = t * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
-                    if (key >= a.Nk) sacc[kb][i] = -INFINITY;
+#pragma unroll
+                    for (int qp = 0; qp < QP; ++qp)
+                        if (key >= a.Nk) sacc[qp][kb][i] = -INFINITY;
                 }
         }
 
-        float mx = -INFINITY;
+        float mc[QP];
 #pragma unroll
-        for (int kb = 0; kb < C::NKB; ++kb)
+        for (int qp = 0; qp < QP; ++qp) {
+            float mx = -INFINITY;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kb][i]);
-        mx = halves_max(mx);
-        if (__builtin_amdgcn_ballot_w64(mx > m_ref + thr) != 0) {
-            const float m_new = fmaxf(m_ref, mx);
-            // m_new = -inf only while a wave has seen no valid key: keep alpha finite
-            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_ref - m_new) * a.c2);
-            m_ref = m_new;
-            l_run *= alpha;
+            for (int kb = 0; kb < C::NKB; ++kb)
 #pragma unroll
-            for (int db = 0; db < C::DBLK; ++db) oacc[db] *= alpha;
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[qp][kb][i]);
+            mx = halves_max(mx);
+            if (__builtin_amdgcn_ballot_w64(mx > m_ref[qp] + thr) != 0) {
+                const float m_new = fmaxf(m_ref[qp], mx);
+                // m_new = -inf only while a wave has seen no valid key: keep alpha finite
+                const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_ref[qp] - m_new) * a.c2);
+                m_ref[qp] = m_new;
+                l_run[qp] *= alpha;
+#pragma unroll
+                for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] *= alpha;
+            }
+            // with no valid key yet every score is -inf and any finite shift gives 0
+            mc[qp] = m_ref[qp] == -INFINITY ? 0.f : m_ref[qp] * a.c2;
         }
-        // with no valid key yet every score is -inf and any finite shift gives 0
-        const float mc = m_ref == -INFINITY ? 0.f : m_ref * a.c2;
 
         // O^T += V^T P^T over KW/16 k-steps of 16 keys.  Each step issues its
         // V^T reads, computes its weights while they are in flight, waits,
@@ -474,22 +500,28 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 }
             });
             constexpr int kb = ks >> 1, i0 = 8 * (ks & 1);
-            float p[8];
+            bf16x8 pb[QP];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i0 + e], a.c2, -mc));
-                if constexpr (!C::SUM_BY_MFMA) l_run += p[e];
+            for (int qp = 0; qp < QP; ++qp) {
+                float p[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[qp][kb][i0 + e], a.c2, -mc[qp]));
+                    if constexpr (!C::SUM_BY_MFMA) l_run[qp] += p[e];
+                }
+                u32x4 pw;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
+                pb[qp] = __builtin_bit_cast(bf16x8, pw);
             }
-            u32x4 pw;
-#pragma unroll
-            for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
-            const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
             lds_wait(vr);
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
                 const u32x4 v4 = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb, oacc[db],
-                                                                   0, 0, 0);
+#pragma unroll
+                for (int qp = 0; qp < QP; ++qp)
+                    oacc[qp][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb[qp],
+                                                                           oacc[qp][db], 0, 0, 0);
             }
         });
     }
@@ -500,72 +532,84 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     if constexpr (KS > 1) {
         float* xs = (float*)lds;
         if (kh > 0) {
-            float* slot = xs + ((kh - 1) * QB + qb) * C::XSLOT;
-            slot[lane] = m_ref;
-            slot[64 + lane] = l_run;
 #pragma unroll
-            for (int db = 0; db < C::DBLK; ++db)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[db][i];
-        }
-        __syncthreads();
-        if (kh == 0) {
-            float M = m_ref;
-#pragma unroll
-            for (int k2 = 1; k2 < KS; ++k2) M = fmaxf(M, xs[((k2 - 1) * QB + qb) * C::XSLOT + lane]);
-            const float mM = M == -INFINITY ? 0.f : M;
-            const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_ref - mM) * a.c2);
-            l_run *= a0;
-#pragma unroll
-            for (int db = 0; db < C::DBLK; ++db) oacc[db] *= a0;
-#pragma unroll
-            for (int k2 = 1; k2 < KS; ++k2) {
-                const float* slot = xs + ((k2 - 1) * QB + qb) * C::XSLOT;
-                const float mk = slot[lane];
-                const float ak = mk == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mk - mM) * a.c2);
-                l_run = __builtin_fmaf(ak, slot[64 + lane], l_run);
+            for (int qp = 0; qp < QP; ++qp) {
+                float* slot = xs + (((kh - 1) * QB + qb) * QP + qp) * C::XSLOT;
+                slot[lane] = m_ref[qp];
+                slot[64 + lane] = l_run[qp];
 #pragma unroll
                 for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        oacc[db][i] = __builtin_fmaf(ak, slot[(2 + 16 * db + i) * 64 + lane], oacc[db][i]);
+                    for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[qp][db][i];
             }
-            m_ref = M;
+        }
+        __syncthreads();
+        if (kh == 0) {
+#pragma unroll
+            for (int qp = 0; qp < QP; ++qp) {
+                float M = m_ref[qp];
+#pragma unroll
+                for (int k2 = 1; k2 < KS; ++k2)
+                    M = fmaxf(M, xs[(((k2 - 1) * QB + qb) * QP + qp) * C::XSLOT + lane]);
+                const float mM = M == -INFINITY ? 0.f : M;
+                const float a0 = m_ref[qp] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_ref[qp] - mM) * a.c2);
+                l_run[qp] *= a0;
+#pragma unroll
+                for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] *= a0;
+#pragma unroll
+                for (int k2 = 1; k2 < KS; ++k2) {
+                    const float* slot = xs + (((k2 - 1) * QB + qb) * QP + qp) * C::XSLOT;
+                    const float mk = slot[lane];
+                    const float ak = mk == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mk - mM) * a.c2);
+                    l_run[qp] = __builtin_fmaf(ak, slot[64 + lane], l_run[qp]);
+#pragma unroll
+                    for (int db = 0; db < C::DBLK; ++db)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            oacc[qp][db][i] = __builtin_fmaf(ak, slot[(2 + 16 * db + i) * 64 + lane], oacc[qp][db][i]);
+                }
+                m_ref[qp] = M;
+            }
         }
     }
     if (kh != 0) return;
 
-    float l_tot;
-    if constexpr (C::SUM_BY_MFMA) {
-        // row D of O^T: block D/32, local row lr held by lanes of half (lr/4)&1
-        constexpr int lr = D % 32, idx = 4 * (lr / 8) + (lr % 4), owner = (lr / 4) & 1;
-        l_tot = __shfl(oacc[D / 32][idx], c + 32 * owner);
-    } else {
-        l_tot = halves_sum(l_run);
-    }
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
-    for (int db = 0; db < C::DBLK; ++db)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            // dims 32db + 8g + 4hf .. +3
-            const int dim = 32 * db + 8 * g + 4 * hf;
-            if (dim < D) {
-                const u32x2 w = {pack_bf16x2(oacc[db][4 * g] * inv, oacc[db][4 * g + 1] * inv),
-                                 pack_bf16x2(oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv)};
-                const uint32_t o = qvalid ? (uint32_t)qrow * rowb + headb + 2 * dim : kOOB;
-                __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
-            }
+    for (int qp = 0; qp < QP; ++qp) {
+        float l_tot;
+        if constexpr (C::SUM_BY_MFMA) {
+            // row D of O^T: block D/32, local row lr held by lanes of half (lr/4)&1
+            constexpr int lr = D % 32, idx = 4 * (lr / 8) + (lr % 4), owner = (lr / 4) & 1;
+            l_tot = __shfl(oacc[qp][D / 32][idx], c + 32 * owner);
+        } else {
+            l_tot = halves_sum(l_run[qp]);
         }
-    if (a.lse && hf == 0 && qvalid) {
-        const float lse = l_tot > 0.f ? (m_ref * a.c2 + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-        a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = lse;
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+#pragma unroll
+        for (int db = 0; db < C::DBLK; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                // dims 32db + 8g + 4hf .. +3
+                const int dim = 32 * db + 8 * g + 4 * hf;
+                if (dim < D) {
+                    const f32x16& o16 = oacc[qp][db];
+                    const u32x2 w = {pack_bf16x2(o16[4 * g] * inv, o16[4 * g + 1] * inv),
+                                     pack_bf16x2(o16[4 * g + 2] * inv, o16[4 * g + 3] * inv)};
+                    const uint32_t o = qvalid[qp] ? (uint32_t)qrow[qp] * rowb + headb + 2 * dim : kOOB;
+                    __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
+                }
+            }
+        if (a.lse && hf == 0 && qvalid[qp]) {
+            const float lse =
+                l_tot > 0.f ? (m_ref[qp] * a.c2 + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+            a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow[qp]] = lse;
+        }
     }
 }
 
-template <int D, int QB, int KS, int KW, bool PATCH>
+template <int D, int QB, int KS, int KW, int QP, bool PATCH>
 hipError_t launch(const AttnParams& p, hipStream_t s) {
-    using C = Cfg<D, QB, KS, KW>;
+    using C = Cfg<D, QB, KS, KW, QP>;
     Args a;
     a.q = (const uint16_t*)p.q;
     a.k = (const uint16_t*)p.k;
@@ -586,14 +630,17 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
+    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, QP, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
                        0, s, a);
     return hipGetLastError();
 }
 
-// Two shapes of 8-wave workgroup: 128 query rows x 2 key splits ("wide"),
-// or 64 query rows x 4 key splits ("narrow") for query counts whose 128-row
-// tiles would leave many of the 256 CUs idle.
+// Shapes of 8-wave workgroup.  "Wide": 128 query rows as 4 query blocks x 2
+// key splits (a 128-key tile at d <= 72, 64 keys at d = 128 for the register
+// budget).  "Narrow": 64 query rows x 4 key splits of a 128-key tile, for
+// query counts whose 128-row tiles would leave many of the 256 CUs idle.
+// "Wide2" (selectable only): 128 rows as 2 groups x 4 key splits, each wave
+// holding two query blocks so every LDS operand read feeds two MFMAs.
 constexpr int kCUs = 256;
 
 double fill(int64_t blocks) {
@@ -601,29 +648,37 @@ double fill(int64_t blocks) {
     return rounds ? (double)blocks / (double)(rounds * kCUs) : 1.0;
 }
 
-// XDIT_ATTN_TILE=wide|narrow forces one shape (tuning and tests); anything
-// else, or unset, picks by the fill estimate below.
+// XDIT_ATTN_TILE forces one shape (tuning and tests): "wide", "narrow", or
+// "wide2" (128 rows as 2 groups x 4 key splits with two query blocks per
+// wave, d <= 72 only); anything else, or unset, picks by the fill estimate.
 int forced_shape() {
     const char* e = getenv("XDIT_ATTN_TILE");
     if (e == nullptr) return 0;
     if (strcmp(e, "wide") == 0) return 1;
     if (strcmp(e, "narrow") == 0) return 2;
+    if (strcmp(e, "wide2") == 0) return 3;
     return 0;
 }
 
 template <int D, bool PATCH>
+hipError_t launch_wide(const AttnParams& p, hipStream_t s) {
+    if constexpr (D > 96) return launch<D, 4, 2, 32, 1, PATCH>(p, s);
+    else return launch<D, 4, 2, 64, 1, PATCH>(p, s);
+}
+
+template <int D, bool PATCH>
 hipError_t dispatch(const AttnParams& p, hipStream_t s) {
-    // keys per wave per tile: 64 at d <= 72, 32 at d = 128 (register budget)
-    constexpr int KWW = D > 96 ? 32 : 64;
     const int forced = forced_shape();
-    if (forced == 1) return launch<D, 4, 2, KWW, PATCH>(p, s);
-    if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
+    if (forced == 1) return launch_wide<D, PATCH>(p, s);
+    if (forced == 2) return launch<D, 2, 4, 32, 1, PATCH>(p, s);
+    if constexpr (D <= 96)
+        if (forced == 3) return launch<D, 2, 4, 32, 2, PATCH>(p, s);
     const int64_t bh = (int64_t)p.B * p.H;
     const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
     const double qfill_w = (double)p.Nq / ((p.Nq + 127) / 128 * 128.0);
     const double qfill_n = (double)p.Nq / ((p.Nq + 63) / 64 * 64.0);
-    if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, PATCH>(p, s);
-    return launch<D, 4, 2, KWW, PATCH>(p, s);
+    if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, 1, PATCH>(p, s);
+    return launch_wide<D, PATCH>(p, s);
 }
 
 }  // namespace

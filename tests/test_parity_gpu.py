@@ -24,10 +24,12 @@ def torch():
     return torch_mod()
 
 
-@pytest.fixture(params=["auto", "wide", "narrow"])
+@pytest.fixture(params=["auto", "wide", "narrow", "wide2"])
 def tile_shape(request, monkeypatch):
     """Workgroup shape of the bf16 kernel: 128 query rows x 2 key splits
-    ("wide"), 64 x 4 ("narrow"), or the library's own choice."""
+    ("wide"), 64 x 4 ("narrow"), 128 x 4 with two query blocks per wave
+    ("wide2", head dim <= 72; larger ones take the library's choice), or the
+    library's own choice."""
     if request.param == "auto":
         monkeypatch.delenv("XDIT_ATTN_TILE", raising=False)
     else:
