@@ -72,12 +72,12 @@ constexpr int kRsrcFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kRescaleLog2 = 8.0f;    // raise the reference max only beyond 2^8 growth
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
 
-template <int D, int QB_, int KS_, int KW_, int QP_>
+template <int D, int QB_, int KS_, int KW_>
 struct Cfg {
-    static constexpr int QB = QB_, KS = KS_, KW = KW_, QP = QP_;
+    static constexpr int QB = QB_, KS = KS_, KW = KW_;
     static constexpr int NW = QB * KS;               // waves per workgroup
     static constexpr int THREADS = 64 * NW;
-    static constexpr int BM = 32 * QP * QB;          // query rows per workgroup
+    static constexpr int BM = 32 * QB;               // query rows per workgroup
     static constexpr int BN = KS * KW;               // keys per tile
     static constexpr int DK = (D + 15) / 16 * 16;    // QK^T contraction length, padded to 16
     static constexpr int DV = (D + 31) / 32 * 32;    // PV output rows, padded to 32
@@ -90,7 +90,9 @@ struct Cfg {
     static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
     static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
-    static constexpr int NSTAGE = kLdsBytes / STAGE_BYTES >= 3 ? 3 : 2;
+    // Iteration t reads V of tile t and K of tile t+1 while the tiles after
+    // them load: three stages at least, four where they fit.
+    static constexpr int NSTAGE = kLdsBytes / STAGE_BYTES >= 4 ? 4 : 3;
     static constexpr int DMA_PER_TILE = TILE_BYTES / 1024;  // 64 lanes x 16 bytes per load
     static constexpr int DMA_PER_WAVE = (DMA_PER_TILE + NW - 1) / NW;
     static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
@@ -100,7 +102,7 @@ struct Cfg {
     // end-of-sweep exchange: one slot (m, l, O^T accumulators) per query
     // block of each partial wave
     static constexpr int XSLOT = 64 * (2 + 16 * DBLK);  // floats
-    static constexpr int X_BYTES = 4 * QB * QP * (KS - 1) * XSLOT;
+    static constexpr int X_BYTES = 4 * QB * (KS - 1) * XSLOT;
     static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES > X_BYTES ? NSTAGE * STAGE_BYTES : X_BYTES;
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
     static_assert(DV - D == 0 || DV - D == 24, "V padding handled for d = 72 only");
@@ -172,18 +174,13 @@ __device__ __forceinline__ u32x2 tr_read(uint32_t a) {
 }
 // Wait for all LDS reads of this wave; the operands are the registers those
 // reads fill, so nothing reads them before the wait.
-template <int N>
-__device__ __forceinline__ void lds_wait(u32x2 (&r)[N][2]) {
-    static_assert(N >= 1 && N <= 4, "up to four operand blocks");
-    if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]));
-    if constexpr (N == 2)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]));
-    if constexpr (N == 3)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]),
-                     "+v"(r[2][0]), "+v"(r[2][1]));
-    if constexpr (N == 4)
-        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0][0]), "+v"(r[0][1]), "+v"(r[1][0]), "+v"(r[1][1]),
-                     "+v"(r[2][0]), "+v"(r[2][1]), "+v"(r[3][0]), "+v"(r[3][1]));
+template <int NS, int NB>
+__device__ __forceinline__ void lds_wait_all(u32x2 (&r)[NS][NB][2]) {
+    asm volatile("s_waitcnt lgkmcnt(0)");
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(r[i][j][0]), "+v"(r[i][j][1]));
 }
 
 __device__ __forceinline__ int xcd_remap(int pid, int total) {
@@ -210,16 +207,16 @@ __device__ __forceinline__ float halves_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QB, int KS, int KW, int QP, bool PATCH>
+template <int D, int QB, int KS, int KW, bool PATCH>
 __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
-    using C = Cfg<D, QB, KS, KW, QP>;
-    constexpr int NT = C::THREADS, BN = C::BN, NST = C::NSTAGE;
+    using C = Cfg<D, QB, KS, KW>;
+    constexpr int NT = C::THREADS, BN = C::BN, NST = C::NSTAGE, NKB = C::NKB, NKS = C::NKS;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int c = lane & 31, hf = lane >> 5;
-    const int qb = wave % QB, kh = wave / QB;  // query-block group, key split
+    const int qb = wave % QB, kh = wave / QB;  // query block, key split
 
     const int logical = xcd_remap(blockIdx.x, gridDim.x);
     const int qt = logical % a.q_tiles;
@@ -269,31 +266,23 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         wait_vmem<0>();
     }
 
-    // The wave's QP blocks of 32 query rows, as B operands (lane: query c,
-    // dims 16kk+8hf..+7).  Each K or V^T operand read from LDS then feeds QP
-    // MFMAs.
-    int qrow[QP];
-    bool qvalid[QP];
+    // The wave's 32 query rows as B operands (lane: query c, dims
+    // 16kk+8hf..+7), held in registers for the whole sweep.
+    const int qrow = qt * C::BM + qb * 32 + c;
+    const bool qvalid = qrow < a.Nq;
     const Rsrc rq = rsrc(a.q + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
     const Rsrc ro = rsrc(a.out + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
-    bf16x8 qf[QP][C::KSTEPS];
+    bf16x8 qf[C::KSTEPS];
 #pragma unroll
-    for (int qp = 0; qp < QP; ++qp) {
-        qrow[qp] = qt * C::BM + (qb * QP + qp) * 32 + c;
-        qvalid[qp] = qrow[qp] < a.Nq;
-#pragma unroll
-        for (int kk = 0; kk < C::KSTEPS; ++kk) {
-            const int col = 16 * kk + 8 * hf;
-            const uint32_t o = (qvalid[qp] && col < D) ? (uint32_t)qrow[qp] * rowb + headb + 2 * col : kOOB;
-            qf[qp][kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
-        }
+    for (int kk = 0; kk < C::KSTEPS; ++kk) {
+        const int col = 16 * kk + 8 * hf;
+        const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
+        qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
     }
     // Make sure the query registers are complete before any tile load, so the
     // loop body never waits on memory operations other than the tile loads.
 #pragma unroll
-    for (int qp = 0; qp < QP; ++qp)
-#pragma unroll
-        for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[qp][kk]));
+    for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
 
     // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
     // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
@@ -387,104 +376,88 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             vaddr[db] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
     }
 
-    f32x16 oacc[QP][C::DBLK];
-    float m_ref[QP], l_run[QP];  // reference max of the raw dot products (this wave's
-                                 // keys); this lane's share of the running sum
+    f32x16 oacc[C::DBLK];
 #pragma unroll
-    for (int qp = 0; qp < QP; ++qp) {
-#pragma unroll
-        for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] = f32x16{};
-        m_ref[qp] = -INFINITY;
-        l_run[qp] = 0.f;
-    }
+    for (int db = 0; db < C::DBLK; ++db) oacc[db] = f32x16{};
+    float m_ref = -INFINITY;  // reference max of the raw dot products (this wave's keys)
+    float l_run = 0.f;        // this lane's share of the running sum
+    float mc = 0.f;           // m_ref * c2, the shift of the exponents
     const float thr = kRescaleLog2 / a.c2;
 
-    __syncthreads();  // the constant chunks are written
-
-    const int ntiles = (a.Nk + BN - 1) / BN;
-#pragma unroll
-    for (int t = 0; t < NST - 1; ++t)
-        if (t < ntiles) load_tile(t, t);
-
-    for (int t = 0; t < ntiles; ++t) {
-        // Tile t must have landed (up to NST-2 younger tiles may still be in
-        // flight) before anyone reads it: each wave waits for its own loads,
-        // then all meet.  A bare s_barrier: the full __syncthreads fence would
-        // also drain the younger loads.  Reads of the stage being refilled
-        // below finished in the previous iteration (their results were
-        // consumed there), so no LDS wait is needed either.
-        const int younger = min(ntiles - 1 - t, NST - 2);
-        if (younger >= 1) wait_vmem<C::DMA_MIN_PER_WAVE>();
-        else wait_vmem<0>();
-        asm volatile("" ::: "memory");  // no LDS access moves across the barrier
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        // everybody is past tile t-1, so its stage takes tile t+NST-1
-        if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
-
+    // S^T of tile t for this wave's KW keys x 32 queries: s[kb][i] = score of
+    // key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against query c.
+    auto qk = [&](int t, f32x16 (&s)[NKB]) {
         const unsigned char* st = stage(t % NST);
-
-        // S^T for this wave's KW keys x 32 queries of block qp: sacc[qp][kb][i]
-        // = score of key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against
-        // query c of the block.
-        f32x16 sacc[QP][C::NKB];
 #pragma unroll
-        for (int qp = 0; qp < QP; ++qp)
-#pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb) sacc[qp][kb] = f32x16{};
+        for (int kb = 0; kb < NKB; ++kb) s[kb] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb) {
+            for (int kb = 0; kb < NKB; ++kb) {
                 uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
                 if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
                 const bf16x8 ka = *(const bf16x8*)(st + ad);
-#pragma unroll
-                for (int qp = 0; qp < QP; ++qp)
-                    sacc[qp][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[qp][kk], sacc[qp][kb], 0, 0, 0);
+                s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s[kb], 0, 0, 0);
             }
-
-        if ((t + 1) * BN > a.Nk) {  // ragged last tile: keys past the end get -inf
+    };
+    // keys past the end of a ragged last tile get -inf
+    auto mask = [&](int t, f32x16 (&s)[NKB]) {
+        if ((t + 1) * BN > a.Nk) {
 #pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb)
+            for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int key = t * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
-#pragma unroll
-                    for (int qp = 0; qp < QP; ++qp)
-                        if (key >= a.Nk) sacc[qp][kb][i] = -INFINITY;
+                    if (key >= a.Nk) s[kb][i] = -INFINITY;
                 }
         }
-
-        float mc[QP];
+    };
+    // Row max of a tile (the same value in both lanes of a query).
+    auto row_max = [&](const f32x16 (&s)[NKB]) -> float {
+        float mx = -INFINITY;
 #pragma unroll
-        for (int qp = 0; qp < QP; ++qp) {
-            float mx = -INFINITY;
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int kb = 0; kb < C::NKB; ++kb)
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
+        return halves_max(mx);
+    };
+    // The reference max is raised (and the running sums rescaled) only if a
+    // tile's max exceeds it by more than 2^8 in weight.
+    auto update_max = [&](float mx) {
+        if (__builtin_amdgcn_ballot_w64(mx > m_ref + thr) != 0) {
+            const float m_new = fmaxf(m_ref, mx);
+            // m_new = -inf only while a wave has seen no valid key: keep alpha finite
+            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_ref - m_new) * a.c2);
+            m_ref = m_new;
+            l_run *= alpha;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[qp][kb][i]);
-            mx = halves_max(mx);
-            if (__builtin_amdgcn_ballot_w64(mx > m_ref[qp] + thr) != 0) {
-                const float m_new = fmaxf(m_ref[qp], mx);
-                // m_new = -inf only while a wave has seen no valid key: keep alpha finite
-                const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_ref[qp] - m_new) * a.c2);
-                m_ref[qp] = m_new;
-                l_run[qp] *= alpha;
-#pragma unroll
-                for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] *= alpha;
-            }
-            // with no valid key yet every score is -inf and any finite shift gives 0
-            mc[qp] = m_ref[qp] == -INFINITY ? 0.f : m_ref[qp] * a.c2;
+            for (int db = 0; db < C::DBLK; ++db) oacc[db] *= alpha;
         }
-
-        // O^T += V^T P^T over KW/16 k-steps of 16 keys.  Each step issues its
-        // V^T reads, computes its weights while they are in flight, waits,
-        // then runs the MFMAs.
+        // with no valid key yet every score is -inf and any finite shift gives 0
+        mc = m_ref == -INFINITY ? 0.f : m_ref * a.c2;
+    };
+    // bf16 weights of a tile, pb[ks] = B operand of 16-key PV step ks
+    auto weights = [&](const f32x16 (&s)[NKB], bf16x8 (&pb)[NKS]) {
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const int kb = ks >> 1, i0 = 8 * (ks & 1);
+            float p[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][i0 + e], a.c2, -mc));
+                if constexpr (!C::SUM_BY_MFMA) l_run += p[e];
+            }
+            u32x4 pw;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
+            pb[ks] = __builtin_bit_cast(bf16x8, pw);
+        }
+    };
+    // V^T operands of tile t, all NKS k-steps, issued without a wait
+    auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2]) {
         const uint32_t vst = lds_u32 + (uint32_t)((t % NST) * C::STAGE_BYTES);
-        static_for<0, C::NKS>([&](auto ksc) {
+        static_for<0, NKS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
-            u32x2 vr[C::DBLK][2];
             static_for<0, C::DBLK>([&](auto dbc) {
                 constexpr int db = decltype(dbc)::value;
                 if constexpr (32 * db + 31 >= D && C::DV > D) {
@@ -492,38 +465,112 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                     const bool cst = vaddr[db] >= (uint32_t)C::CONST_OFF;
                     const uint32_t a0 = vst + vaddr[db] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
                     const uint32_t a1 = vst + vaddr[db] + (cst ? 0u : (uint32_t)((16 * ks + 8) * C::ROWB));
-                    vr[db][0] = tr_read<0>(a0);
-                    vr[db][1] = tr_read<0>(a1);
+                    vr[ks][db][0] = tr_read<0>(a0);
+                    vr[ks][db][1] = tr_read<0>(a1);
                 } else {
-                    vr[db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db]);
-                    vr[db][1] = tr_read<(16 * ks + 8) * C::ROWB>(vst + vaddr[db]);
+                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db]);
+                    vr[ks][db][1] = tr_read<(16 * ks + 8) * C::ROWB>(vst + vaddr[db]);
                 }
             });
-            constexpr int kb = ks >> 1, i0 = 8 * (ks & 1);
-            bf16x8 pb[QP];
+        });
+    };
+    // O^T += V^T P^T over the NKS k-steps
+    auto pv = [&](const u32x2 (&vr)[NKS][C::DBLK][2], const bf16x8 (&pb)[NKS]) {
 #pragma unroll
-            for (int qp = 0; qp < QP; ++qp) {
-                float p[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[qp][kb][i0 + e], a.c2, -mc[qp]));
-                    if constexpr (!C::SUM_BY_MFMA) l_run[qp] += p[e];
-                }
-                u32x4 pw;
-#pragma unroll
-                for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
-                pb[qp] = __builtin_bit_cast(bf16x8, pw);
-            }
-            lds_wait(vr);
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
-                const u32x4 v4 = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
-#pragma unroll
-                for (int qp = 0; qp < QP; ++qp)
-                    oacc[qp][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb[qp],
-                                                                           oacc[qp][db], 0, 0, 0);
+                const u32x4 v4 = {vr[ks][db][0][0], vr[ks][db][0][1], vr[ks][db][1][0], vr[ks][db][1][1]};
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb[ks], oacc[db],
+                                                                   0, 0, 0);
             }
-        });
+    };
+
+    // Wait until at most the loads of the N most recently issued tiles are in
+    // flight.  A wave issues the same number of loads for every tile (twice
+    // as many for a tile that straddles the slice edge, which only makes the
+    // wait stricter): 2*DMA_PER_WAVE if it takes one of the leftover 1 KiB
+    // pieces of a tile, 2*(DMA_PER_TILE / NW) otherwise.
+    const bool extra_piece = wave + (C::DMA_PER_WAVE - 1) * C::NW < C::DMA_PER_TILE;
+    auto wait_tiles = [&](auto n_c) {
+        constexpr int N = decltype(n_c)::value;
+        if (C::DMA_PER_TILE % C::NW != 0 && extra_piece) wait_vmem<N * 2 * C::DMA_PER_WAVE>();
+        else wait_vmem<N * C::DMA_MIN_PER_WAVE>();
+    };
+
+    // Software pipeline: iteration t computes the weights and PV of tile t
+    // and, on the matrix cores meanwhile, the scores of tile t+1; the row
+    // max of tile t+1 then runs under the PV products.  Scores of tile t
+    // live in sc, those of tile t+1 go to sn.  NEXT: there is a tile t+1;
+    // MASK: it may be the ragged last tile.
+    const int ntiles = (a.Nk + BN - 1) / BN;
+    auto iteration = [&](int t, f32x16 (&sc)[NKB], f32x16 (&sn)[NKB], auto next_c, auto mask_c) {
+        constexpr bool NEXT = decltype(next_c)::value, MASK = decltype(mask_c)::value;
+        if constexpr (NEXT) {
+            // Tile t+1 must have landed (tile t+2 may still be in flight with
+            // four stages) before anyone reads it: each wave waits for its own
+            // loads, then all meet.  A bare s_barrier: the full __syncthreads
+            // fence would also drain the younger loads.  Everybody is then
+            // done with tile t-1 (its V was read in the previous iteration,
+            // its K in the one before), so its stage takes tile t+NST-1.
+            if (NST >= 4 && t + 2 < ntiles) wait_tiles(std::integral_constant<int, 1>{});
+            else wait_vmem<0>();
+            asm volatile("" ::: "memory");  // no LDS access moves across the barrier
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
+        }
+        u32x2 vr[NKS][C::DBLK][2];
+        read_vt(t, vr);
+        bf16x8 pb[NKS];
+        weights(sc, pb);
+        float mx = 0.f;
+        if constexpr (NEXT) {
+            qk(t + 1, sn);
+            if constexpr (MASK) mask(t + 1, sn);
+            mx = row_max(sn);
+        }
+        lds_wait_all(vr);
+        pv(vr, pb);
+        if constexpr (NEXT) update_max(mx);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+
+    __syncthreads();  // the constant chunks are written
+
+    f32x16 sA[NKB], sB[NKB];
+    if (ntiles > 0) {
+#pragma unroll
+        for (int t = 0; t < NST - 1; ++t)
+            if (t < ntiles) load_tile(t, t);
+        // tile 0 must have landed; up to NST-2 younger tiles may be in flight
+        if (NST >= 4 && ntiles >= 3) wait_tiles(std::integral_constant<int, 2>{});
+        else if (ntiles >= 2) wait_tiles(std::integral_constant<int, 1>{});
+        else wait_vmem<0>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        qk(0, sA);
+        mask(0, sA);
+        update_max(row_max(sA));
+    }
+    // pairs of iterations whose next tile is not the last one, then the
+    // last one to three tiles
+    int t = 0;
+    for (; t + 3 < ntiles; t += 2) {
+        iteration(t, sA, sB, T_{}, F_{});
+        iteration(t + 1, sB, sA, T_{}, F_{});
+    }
+    if (t + 3 == ntiles) {
+        iteration(t, sA, sB, T_{}, F_{});
+        iteration(t + 1, sB, sA, T_{}, T_{});
+        iteration(t + 2, sA, sB, F_{}, F_{});
+    } else if (t + 2 == ntiles) {
+        iteration(t, sA, sB, T_{}, T_{});
+        iteration(t + 1, sB, sA, F_{}, F_{});
+    } else if (t + 1 == ntiles) {
+        iteration(t, sA, sB, F_{}, F_{});
     }
     __syncthreads();  // every wave is done with the stages
 
@@ -532,84 +579,73 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     if constexpr (KS > 1) {
         float* xs = (float*)lds;
         if (kh > 0) {
+            float* slot = xs + ((kh - 1) * QB + qb) * C::XSLOT;
+            slot[lane] = m_ref;
+            slot[64 + lane] = l_run;
 #pragma unroll
-            for (int qp = 0; qp < QP; ++qp) {
-                float* slot = xs + (((kh - 1) * QB + qb) * QP + qp) * C::XSLOT;
-                slot[lane] = m_ref[qp];
-                slot[64 + lane] = l_run[qp];
+            for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
-                for (int db = 0; db < C::DBLK; ++db)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[qp][db][i];
-            }
+                for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[db][i];
         }
         __syncthreads();
         if (kh == 0) {
+            float M = m_ref;
 #pragma unroll
-            for (int qp = 0; qp < QP; ++qp) {
-                float M = m_ref[qp];
+            for (int k2 = 1; k2 < KS; ++k2) M = fmaxf(M, xs[((k2 - 1) * QB + qb) * C::XSLOT + lane]);
+            const float mM = M == -INFINITY ? 0.f : M;
+            const float a0 = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_ref - mM) * a.c2);
+            l_run *= a0;
 #pragma unroll
-                for (int k2 = 1; k2 < KS; ++k2)
-                    M = fmaxf(M, xs[(((k2 - 1) * QB + qb) * QP + qp) * C::XSLOT + lane]);
-                const float mM = M == -INFINITY ? 0.f : M;
-                const float a0 = m_ref[qp] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_ref[qp] - mM) * a.c2);
-                l_run[qp] *= a0;
+            for (int db = 0; db < C::DBLK; ++db) oacc[db] *= a0;
 #pragma unroll
-                for (int db = 0; db < C::DBLK; ++db) oacc[qp][db] *= a0;
+            for (int k2 = 1; k2 < KS; ++k2) {
+                const float* slot = xs + ((k2 - 1) * QB + qb) * C::XSLOT;
+                const float mk = slot[lane];
+                const float ak = mk == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mk - mM) * a.c2);
+                l_run = __builtin_fmaf(ak, slot[64 + lane], l_run);
 #pragma unroll
-                for (int k2 = 1; k2 < KS; ++k2) {
-                    const float* slot = xs + (((k2 - 1) * QB + qb) * QP + qp) * C::XSLOT;
-                    const float mk = slot[lane];
-                    const float ak = mk == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((mk - mM) * a.c2);
-                    l_run[qp] = __builtin_fmaf(ak, slot[64 + lane], l_run[qp]);
+                for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
-                    for (int db = 0; db < C::DBLK; ++db)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            oacc[qp][db][i] = __builtin_fmaf(ak, slot[(2 + 16 * db + i) * 64 + lane], oacc[qp][db][i]);
-                }
-                m_ref[qp] = M;
+                    for (int i = 0; i < 16; ++i)
+                        oacc[db][i] = __builtin_fmaf(ak, slot[(2 + 16 * db + i) * 64 + lane], oacc[db][i]);
             }
+            m_ref = M;
         }
     }
     if (kh != 0) return;
 
+    float l_tot;
+    if constexpr (C::SUM_BY_MFMA) {
+        // row D of O^T: block D/32, local row lr held by lanes of half (lr/4)&1
+        constexpr int lr = D % 32, idx = 4 * (lr / 8) + (lr % 4), owner = (lr / 4) & 1;
+        l_tot = __shfl(oacc[D / 32][idx], c + 32 * owner);
+    } else {
+        l_tot = halves_sum(l_run);
+    }
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
-    for (int qp = 0; qp < QP; ++qp) {
-        float l_tot;
-        if constexpr (C::SUM_BY_MFMA) {
-            // row D of O^T: block D/32, local row lr held by lanes of half (lr/4)&1
-            constexpr int lr = D % 32, idx = 4 * (lr / 8) + (lr % 4), owner = (lr / 4) & 1;
-            l_tot = __shfl(oacc[qp][D / 32][idx], c + 32 * owner);
-        } else {
-            l_tot = halves_sum(l_run[qp]);
-        }
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
-        for (int db = 0; db < C::DBLK; ++db)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                // dims 32db + 8g + 4hf .. +3
-                const int dim = 32 * db + 8 * g + 4 * hf;
-                if (dim < D) {
-                    const f32x16& o16 = oacc[qp][db];
-                    const u32x2 w = {pack_bf16x2(o16[4 * g] * inv, o16[4 * g + 1] * inv),
-                                     pack_bf16x2(o16[4 * g + 2] * inv, o16[4 * g + 3] * inv)};
-                    const uint32_t o = qvalid[qp] ? (uint32_t)qrow[qp] * rowb + headb + 2 * dim : kOOB;
-                    __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
-                }
+        for (int g = 0; g < 4; ++g) {
+            // dims 32db + 8g + 4hf .. +3
+            const int dim = 32 * db + 8 * g + 4 * hf;
+            if (dim < D) {
+                const f32x16& o16 = oacc[db];
+                const u32x2 w = {pack_bf16x2(o16[4 * g] * inv, o16[4 * g + 1] * inv),
+                                 pack_bf16x2(o16[4 * g + 2] * inv, o16[4 * g + 3] * inv)};
+                const uint32_t o = qvalid ? (uint32_t)qrow * rowb + headb + 2 * dim : kOOB;
+                __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
             }
-        if (a.lse && hf == 0 && qvalid[qp]) {
-            const float lse =
-                l_tot > 0.f ? (m_ref[qp] * a.c2 + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-            a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow[qp]] = lse;
         }
+    if (a.lse && hf == 0 && qvalid) {
+        const float lse = l_tot > 0.f ? (m_ref * a.c2 + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+        a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = lse;
     }
 }
 
-template <int D, int QB, int KS, int KW, int QP, bool PATCH>
+template <int D, int QB, int KS, int KW, bool PATCH>
 hipError_t launch(const AttnParams& p, hipStream_t s) {
-    using C = Cfg<D, QB, KS, KW, QP>;
+    using C = Cfg<D, QB, KS, KW>;
     Args a;
     a.q = (const uint16_t*)p.q;
     a.k = (const uint16_t*)p.k;
@@ -630,17 +666,16 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, QP, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
+    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
                        0, s, a);
     return hipGetLastError();
 }
 
 // Shapes of 8-wave workgroup.  "Wide": 128 query rows as 4 query blocks x 2
 // key splits (a 128-key tile at d <= 72, 64 keys at d = 128 for the register
-// budget).  "Narrow": 64 query rows x 4 key splits of a 128-key tile, for
-// query counts whose 128-row tiles would leave many of the 256 CUs idle.
-// "Wide2" (selectable only): 128 rows as 2 groups x 4 key splits, each wave
-// holding two query blocks so every LDS operand read feeds two MFMAs.
+// and LDS budget).  "Narrow" (d <= 72): 64 query rows x 4 key splits of a
+// 128-key tile, for query counts whose 128-row tiles would leave many of the
+// 256 CUs idle.
 constexpr int kCUs = 256;
 
 double fill(int64_t blocks) {
@@ -648,37 +683,32 @@ double fill(int64_t blocks) {
     return rounds ? (double)blocks / (double)(rounds * kCUs) : 1.0;
 }
 
-// XDIT_ATTN_TILE forces one shape (tuning and tests): "wide", "narrow", or
-// "wide2" (128 rows as 2 groups x 4 key splits with two query blocks per
-// wave, d <= 72 only); anything else, or unset, picks by the fill estimate.
+// XDIT_ATTN_TILE forces one shape (tuning and tests): "wide" or "narrow"
+// (narrow falls back to wide at d = 128); anything else, or unset, picks by
+// the fill estimate.
 int forced_shape() {
     const char* e = getenv("XDIT_ATTN_TILE");
     if (e == nullptr) return 0;
     if (strcmp(e, "wide") == 0) return 1;
     if (strcmp(e, "narrow") == 0) return 2;
-    if (strcmp(e, "wide2") == 0) return 3;
     return 0;
 }
 
 template <int D, bool PATCH>
-hipError_t launch_wide(const AttnParams& p, hipStream_t s) {
-    if constexpr (D > 96) return launch<D, 4, 2, 32, 1, PATCH>(p, s);
-    else return launch<D, 4, 2, 64, 1, PATCH>(p, s);
-}
-
-template <int D, bool PATCH>
 hipError_t dispatch(const AttnParams& p, hipStream_t s) {
-    const int forced = forced_shape();
-    if (forced == 1) return launch_wide<D, PATCH>(p, s);
-    if (forced == 2) return launch<D, 2, 4, 32, 1, PATCH>(p, s);
-    if constexpr (D <= 96)
-        if (forced == 3) return launch<D, 2, 4, 32, 2, PATCH>(p, s);
-    const int64_t bh = (int64_t)p.B * p.H;
-    const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
-    const double qfill_w = (double)p.Nq / ((p.Nq + 127) / 128 * 128.0);
-    const double qfill_n = (double)p.Nq / ((p.Nq + 63) / 64 * 64.0);
-    if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, 1, PATCH>(p, s);
-    return launch_wide<D, PATCH>(p, s);
+    if constexpr (D > 96) {
+        return launch<D, 4, 2, 32, PATCH>(p, s);
+    } else {
+        const int forced = forced_shape();
+        if (forced == 1) return launch<D, 4, 2, 64, PATCH>(p, s);
+        if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
+        const int64_t bh = (int64_t)p.B * p.H;
+        const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
+        const double qfill_w = (double)p.Nq / ((p.Nq + 127) / 128 * 128.0);
+        const double qfill_n = (double)p.Nq / ((p.Nq + 63) / 64 * 64.0);
+        if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, PATCH>(p, s);
+        return launch<D, 4, 2, 64, PATCH>(p, s);
+    }
 }
 
 }  // namespace

@@ -24,12 +24,11 @@ def torch():
     return torch_mod()
 
 
-@pytest.fixture(params=["auto", "wide", "narrow", "wide2"])
+@pytest.fixture(params=["auto", "wide", "narrow"])
 def tile_shape(request, monkeypatch):
     """Workgroup shape of the bf16 kernel: 128 query rows x 2 key splits
-    ("wide"), 64 x 4 ("narrow"), 128 x 4 with two query blocks per wave
-    ("wide2", head dim <= 72; larger ones take the library's choice), or the
-    library's own choice."""
+    ("wide"), 64 x 4 ("narrow", head dim <= 72; d = 128 always runs wide), or
+    the library's own choice."""
     if request.param == "auto":
         monkeypatch.delenv("XDIT_ATTN_TILE", raising=False)
     else:
@@ -57,6 +56,13 @@ CHUNK_CASES = [
     ("bf16", 1, 1, 1, 1, 64),
     ("bf16", 1, 5, 64, 1, 72),
     ("bf16", 1, 128, 128, 1, 128),
+    # K/V tile counts 3..11, whole and ragged (tiles of 128 keys at d <= 72,
+    # 64 at d = 128), so that every way the tile loop can end is taken
+    ("bf16", 1, 40, 384, 1, 64),
+    ("bf16", 1, 100, 512, 2, 64),
+    ("bf16", 1, 70, 645, 2, 72),
+    ("bf16", 2, 33, 896, 2, 72),
+    ("bf16", 1, 64, 700, 1, 128),
     ("f32", 1, 256, 256, 2, 64),
     ("f32", 2, 70, 97, 3, 72),
     ("f32", 1, 65, 33, 2, 128),
