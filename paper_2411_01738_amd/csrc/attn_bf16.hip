@@ -520,13 +520,16 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             asm volatile("" ::: "memory");
             if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
         }
-        u32x2 vr[NKS][C::DBLK][2];
-        read_vt(t, vr);
+        // the K operand reads of tile t+1 go first: LDS reads complete in
+        // issue order, so V^T reads issued before them would hold the QK
+        // products back behind the whole V^T batch
         bf16x8 pb[NKS];
         weights(sc, pb);
+        if constexpr (NEXT) qk(t + 1, sn);
+        u32x2 vr[NKS][C::DBLK][2];
+        read_vt(t, vr);
         float mx = 0.f;
         if constexpr (NEXT) {
-            qk(t + 1, sn);
             if constexpr (MASK) mask(t + 1, sn);
             mx = row_max(sn);
         }
