@@ -248,24 +248,6 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             (tid & 1) ? u32x4{0x3f80u, 0, 0, 0} : u32x4{0, 0, 0, 0};
     }
 
-    // Patch mode: this workgroup's share of the fresh slice goes into the
-    // buffer (all query tiles of a (batch, head) split the rows).  Nobody
-    // reads the slice rows of the buffer: they are taken from the fresh rows.
-    if constexpr (PATCH) {
-        const int r0 = (int)((int64_t)a.len * qt / a.q_tiles);
-        const int r1 = (int)((int64_t)a.len * (qt + 1) / a.q_tiles);
-        const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
-        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), a.off, a.Nk);
-        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), a.off, a.Nk);
-        for (int e = tid; e < (r1 - r0) * C::CH; e += NT) {
-            const int r = r0 + e / C::CH;
-            const uint32_t o = (uint32_t)r * rowb + 16 * (e % C::CH);
-            bstore(wk, o, bload(fk, o));
-            bstore(wv, o, bload(fv, o));
-        }
-        wait_vmem<0>();
-    }
-
     // The wave's 32 query rows as B operands (lane: query c, dims
     // 16kk+8hf..+7), held in registers for the whole sweep.
     const int qrow = qt * C::BM + qb * 32 + c;
@@ -279,10 +261,37 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
         qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
     }
-    // Make sure the query registers are complete before any tile load, so the
-    // loop body never waits on memory operations other than the tile loads.
+    // Patch mode: this workgroup's share of the fresh slice goes into the
+    // buffer (all query tiles of a (batch, head) split the rows).  Nobody
+    // reads the slice rows of the buffer: they are taken from the fresh rows.
+    if constexpr (PATCH) {
+        const int r0 = (int)((int64_t)a.len * qt / a.q_tiles);
+        const int r1 = (int)((int64_t)a.len * (qt + 1) / a.q_tiles);
+        const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
+        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), a.off, a.Nk);
+        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), a.off, a.Nk);
+        // a workgroup's share is at most BM rows (q_tiles = ceil(len / BM)):
+        // all loads first, then all stores; chunks past the share use the
+        // out-of-range offset (reads give zero, writes are dropped)
+        constexpr int U = (C::BM * C::CH + NT - 1) / NT;
+        uint32_t co[U];
+        u32x4 ck[U], cv[U];
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
+        for (int u = 0; u < U; ++u) {
+            const int e = tid + u * NT;
+            co[u] = e < (r1 - r0) * C::CH ? (uint32_t)(r0 + e / C::CH) * rowb + 16 * (e % C::CH) : kOOB;
+            ck[u] = bload(fk, co[u]);
+            cv[u] = bload(fv, co[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            bstore(wk, co[u], ck[u]);
+            bstore(wv, co[u], cv[u]);
+        }
+        // no wait: the stores are older than every tile load, and vector
+        // memory operations of a wave complete in issue order, so the first
+        // tile wait below covers them
+    }
 
     // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
     // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
@@ -540,18 +549,23 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     using T_ = std::true_type;
     using F_ = std::false_type;
 
-    __syncthreads();  // the constant chunks are written
-
     f32x16 sA[NKB], sB[NKB];
     if (ntiles > 0) {
 #pragma unroll
         for (int t = 0; t < NST - 1; ++t)
             if (t < ntiles) load_tile(t, t);
-        // tile 0 must have landed; up to NST-2 younger tiles may be in flight
+        // the query loads (issued first) complete while the tiles load; the
+        // loop body then never waits on memory operations other than tile
+        // loads
+#pragma unroll
+        for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
+        // tile 0 must have landed (up to NST-2 younger tiles may be in
+        // flight) and the constant chunks must be written before anyone
+        // reads them
         if (NST >= 4 && ntiles >= 3) wait_tiles(std::integral_constant<int, 2>{});
         else if (ntiles >= 2) wait_tiles(std::integral_constant<int, 1>{});
         else wait_vmem<0>();
-        asm volatile("" ::: "memory");
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         qk(0, sA);
