@@ -41,7 +41,10 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # (FETCH x 1.9944, WRITE x 1.0).  Each entry holds the sha256 prefix of the
 # kernel source it was taken on; a different source reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (51935 + 13826) * 1024, "src": "a211186b2a998c9c"},
+    ("pixart", "patch_attn"): {"bytes": (51597 + 13845) * 1024, "src": "52e15906ea183741"},
+    ("sd3", "patch_attn"): {"bytes": (59291 + 9216) * 1024, "src": "52e15906ea183741"},
+    ("flux", "chunk_attn"): {"bytes": (116118 + 25747) * 1024, "src": "52e15906ea183741"},
+    ("cog", "patch_attn"): {"bytes": (265506 + 19744) * 1024, "src": "52e15906ea183741"},
 }
 
 
