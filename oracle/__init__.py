@@ -64,6 +64,10 @@ class Oracle:
         lib.xo_patch.restype = ctypes.c_int
         lib.xo_patch.argtypes = [_f32p, _f32p, _i64, _i64, _f32p, _f32p, _i64, _i64, _i64, _i64,
                                  ctypes.c_void_p, _i64, _f64p, ctypes.c_void_p]
+        lib.xo_patch_ranges.restype = ctypes.c_int
+        lib.xo_patch_ranges.argtypes = [_f32p, _i64, _f32p, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_void_p, _f32p, _f32p, _i64, _i64, _i64, _i64,
+                                        ctypes.c_void_p, _i64, _f64p, ctypes.c_void_p]
         lib.xo_num_threads.restype = ctypes.c_int
         lib.xo_set_num_threads.argtypes = [ctypes.c_int]
         self.lib = lib
@@ -165,6 +169,37 @@ class Oracle:
                                rows_ptr, nrows, out, lse.ctypes.data)
         if rc:
             raise ValueError("xo_patch rejected its arguments")
+        return out, lse
+
+    def patch_ranges(self, q, kv_buf, ranges, fresh_k, fresh_v, rows=None):
+        """Patch step with fresh rows over several disjoint row ranges
+        [(off, len), ...] of kv_buf [2,B,N,H,d] (float32, in place; fresh_k/v
+        [B, sum(len), H, d] hold the ranges' rows in range order) and its own
+        queries q [B,Nq,H,d].  Returns (out, lse) as attention() does."""
+        if kv_buf.dtype != np.float32 or not kv_buf.flags.c_contiguous:
+            raise TypeError("kv_buf must be a C-contiguous float32 array")
+        q, fresh_k, fresh_v = self._f32(q), self._f32(fresh_k), self._f32(fresh_v)
+        _, B, N, H, d = kv_buf.shape
+        offs = np.ascontiguousarray(np.array([r[0] for r in ranges], dtype=np.int64))
+        lens = np.ascontiguousarray(np.array([r[1] for r in ranges], dtype=np.int64))
+        F = int(lens.sum())
+        if fresh_k.shape != (B, F, H, d) or fresh_v.shape != fresh_k.shape:
+            raise ValueError("fresh K/V shape mismatch")
+        if q.shape[0] != B or q.shape[2:] != (H, d):
+            raise ValueError("q shape mismatch")
+        Nq = q.shape[1]
+        if rows is None:
+            rows_arr, rows_ptr, nrows = None, None, Nq
+        else:
+            rows_arr = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+            rows_ptr, nrows = rows_arr.ctypes.data, rows_arr.size
+        out = np.zeros((B, nrows, H, d), np.float64)
+        lse = np.zeros((B, H, nrows), np.float64)
+        rc = self.lib.xo_patch_ranges(q, Nq, kv_buf, len(ranges), offs.ctypes.data,
+                                      lens.ctypes.data, fresh_k, fresh_v, B, N, H, d, rows_ptr,
+                                      nrows, out, lse.ctypes.data)
+        if rc:
+            raise ValueError("xo_patch_ranges rejected its arguments")
         return out, lse
 
 

@@ -206,3 +206,48 @@ int xo_patch(const float* q, float* kv_buf, int64_t off, int64_t len, const floa
     return xo_attention(q, kv_buf, kv_buf + B * N * H * d, B, len, N, H, d, rows, nrows, out,
                         lse);
 }
+
+/*
+ * Patch step with up to several fresh row ranges and its own query rows.
+ *
+ * Section 4.1.2: with in-context conditioning the text tokens travel with
+ * patch 0, so that micro-step refreshes two row ranges of the buffer (the
+ * patch's image rows and the text rows) and its queries are the rows of both.
+ * Section 4.1.4: in hybrid parallelism the K/V a PipeFusion stage stores are
+ * the ones gathered over its sequence-parallel group, while its queries are
+ * only the local shard.
+ *
+ * fresh_k / fresh_v [B, F, H, d], F = sum of lens, hold the ranges' rows in
+ * range order: range r takes fresh rows base_r .. base_r + len_r - 1 with
+ * base_r = len_0 + ... + len_{r-1}.  Ranges must lie in [0, N) and be
+ * disjoint.  After the update, q [B, Nq, H, d] attends over the whole buffer;
+ * rows/nrows/out/lse as in xo_attention (rows index q).
+ */
+int xo_patch_ranges(const float* q, int64_t Nq, float* kv_buf, int32_t nr, const int64_t* offs,
+                    const int64_t* lens, const float* fresh_k, const float* fresh_v, int64_t B,
+                    int64_t N, int64_t H, int64_t d, const int64_t* rows, int64_t nrows, double* out,
+                    double* lse) {
+    if (nr < 0 || Nq < 0 || B < 0 || H < 0 || d <= 0) return -1;
+    int64_t F = 0;
+    for (int32_t r = 0; r < nr; ++r) {
+        if (offs[r] < 0 || lens[r] < 0 || offs[r] + lens[r] > N) return -1;
+        for (int32_t s = 0; s < r; ++s)
+            if (offs[r] < offs[s] + lens[s] && offs[s] < offs[r] + lens[r]) return -1;
+        F += lens[r];
+    }
+    const int64_t plane = B * N * H * d;
+    int64_t base = 0;
+    for (int32_t r = 0; r < nr; ++r) {
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t i = 0; i < lens[r]; ++i)
+                for (int64_t h = 0; h < H; ++h)
+                    for (int64_t c = 0; c < d; ++c) {
+                        const int64_t dst = IDX4(b, offs[r] + i, h, c, N, H, d);
+                        const int64_t src = IDX4(b, base + i, h, c, F, H, d);
+                        kv_buf[dst] = fresh_k[src];
+                        kv_buf[plane + dst] = fresh_v[src];
+                    }
+        base += lens[r];
+    }
+    return xo_attention(q, kv_buf, kv_buf + plane, B, Nq, N, H, d, rows, nrows, out, lse);
+}

@@ -319,6 +319,94 @@ def pin_patch_semantics(orc):
     _close(o, o_full[:, (M - 1) * L:], 0.0, "last patch equals fresh attention")
 
 
+# --------------------------------------------------------------------------
+# patch step over several fresh ranges with its own queries (Section 4.1.2:
+# in-context text travels with patch 0; Section 4.1.4: hybrid parallelism
+# stores SP-gathered K/V and attends with the local query shard)
+# --------------------------------------------------------------------------
+def pin_patch_ranges_brute_force(orc):
+    """Two fresh ranges on a tiny buffer against the direct definition: the
+    buffer rows are rebuilt by hand, row by row, and attention is the brute
+    force softmax (no max shift, math.fsum)."""
+    B, N, H, d = 1, 12, 2, 4
+    kv = np.stack([_rand((B, N, H, d), 111), _rand((B, N, H, d), 112)])
+    before = kv.copy()
+    ranges = [(1, 3), (9, 3)]
+    fk, fv = _rand((B, 6, H, d), 113), _rand((B, 6, H, d), 114)
+    q = _rand((B, 5, H, d), 115)
+    o, l = orc.patch_ranges(q, kv, ranges, fk, fv)
+    k_ref, v_ref = before[0].copy(), before[1].copy()
+    src = 0
+    for off, ln in ranges:
+        for i in range(ln):
+            k_ref[:, off + i] = fk[:, src]
+            v_ref[:, off + i] = fv[:, src]
+            src += 1
+    assert np.array_equal(kv[0], k_ref) and np.array_equal(kv[1], v_ref), "buffer after the update"
+    ob, lb = brute_attention(q, k_ref, v_ref)
+    _close(o, ob, TOL, "two-range patch out")
+    _close(l, lb, TOL, "two-range patch lse")
+
+
+def pin_patch_ranges_in_context(orc):
+    """Patch 0 carrying the text (image rows [0, n_img), text rows after them):
+    one step refreshes patch 0 and the text rows; the image patches after it
+    stay stale; text and patch-0 queries both see the fresh rows.  With M = 1
+    (one patch = the whole image) the step is plain attention over the fresh
+    sequence."""
+    B, H, d, n_img, n_txt, M = 1, 2, 8, 12, 4, 3
+    N, L = n_img + n_txt, n_img // M
+    q = _rand((B, N, H, d), 121)
+    kf, vf = _rand((B, N, H, d), 122), _rand((B, N, H, d), 123)
+    ks = kf + np.float32(0.05) * _rand((B, N, H, d), 124)
+    vs = vf + np.float32(0.05) * _rand((B, N, H, d), 125)
+    rows = np.r_[0:L, n_img:N]
+    kv = np.stack([ks, vs]).copy()
+    o, l = orc.patch_ranges(q[:, rows].copy(), kv, [(0, L), (n_img, n_txt)],
+                            kf[:, rows].copy(), vf[:, rows].copy())
+    fresh = np.zeros(N, bool)
+    fresh[rows] = True
+    assert np.array_equal(kv[0][:, fresh], kf[:, fresh]) and np.array_equal(kv[0][:, ~fresh], ks[:, ~fresh])
+    assert np.array_equal(kv[1][:, fresh], vf[:, fresh]) and np.array_equal(kv[1][:, ~fresh], vs[:, ~fresh])
+    ob, lb = brute_attention(q[:, rows], np.where(fresh[None, :, None, None], kf, ks),
+                             np.where(fresh[None, :, None, None], vf, vs))
+    _close(o, ob, TOL, "in-context patch 0 out")
+    _close(l, lb, TOL, "in-context patch 0 lse")
+    kv = np.stack([ks, vs]).copy()
+    o1, l1 = orc.patch_ranges(q, kv, [(0, n_img), (n_img, n_txt)], kf, vf)
+    of, lf = brute_attention(q, kf, vf)
+    _close(o1, of, TOL, "single patch with text = fresh attention")
+    _close(l1, lf, TOL, "single patch with text lse")
+
+
+def pin_patch_ranges_sp_shards(orc):
+    """Hybrid SP x PipeFusion at one GPU's share: every SP rank stores the
+    same gathered fresh K/V and attends with its own shard of the patch's
+    queries; the ranks' buffers end identical and their outputs, put side by
+    side, are the unsharded step's (here against brute force)."""
+    B, N, H, d, sp = 1, 16, 2, 4, 4
+    kv0 = np.stack([_rand((B, N, H, d), 131), _rand((B, N, H, d), 132)])
+    off, ln = 4, 8
+    fk, fv = _rand((B, ln, H, d), 133), _rand((B, ln, H, d), 134)
+    q = _rand((B, ln, H, d), 135)
+    outs, lses, bufs = [], [], []
+    for r in range(sp):
+        kv = kv0.copy()
+        sh = slice(r * ln // sp, (r + 1) * ln // sp)
+        o, l = orc.patch_ranges(q[:, sh].copy(), kv, [(off, ln)], fk, fv)
+        outs.append(o)
+        lses.append(l)
+        bufs.append(kv)
+    for kv in bufs[1:]:
+        assert np.array_equal(kv, bufs[0]), "SP ranks' buffers differ"
+    k_ref, v_ref = kv0[0].copy(), kv0[1].copy()
+    k_ref[:, off:off + ln], v_ref[:, off:off + ln] = fk, fv
+    ob, lb = brute_attention(q, k_ref, v_ref)
+    _close(np.concatenate(outs, axis=1), ob, TOL, "sharded queries out")
+    _close(np.concatenate(lses, axis=2), lb, TOL, "sharded queries lse")
+
+
 PINS = [pin_brute_force, pin_scipy_softmax, pin_closed_forms, pin_empty_and_rows,
         pin_permutation_and_independence, pin_merge_equals_full, pin_merge_algebra,
-        pin_patch_update_exact, pin_patch_semantics]
+        pin_patch_update_exact, pin_patch_semantics, pin_patch_ranges_brute_force,
+        pin_patch_ranges_in_context, pin_patch_ranges_sp_shards]

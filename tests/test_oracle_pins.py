@@ -48,6 +48,13 @@ MUTANTS = [
      "fresh_k[IDX4(b, i, h, c, len, H, d)];"),
     ("patch skips its update", "int rc = xo_patch_update(kv_buf, off, len,",
      "int rc = xo_patch_update(kv_buf, off, 0,"),
+    ("every range takes the first fresh rows", "const int64_t src = IDX4(b, base + i, h, c, F, H, d);",
+     "const int64_t src = IDX4(b, i, h, c, F, H, d);"),
+    ("last range not stored", "    for (int32_t r = 0; r < nr; ++r) {\n        for (int64_t b = 0; b < B; ++b)",
+     "    for (int32_t r = 0; r < nr - 1; ++r) {\n        for (int64_t b = 0; b < B; ++b)"),
+    ("ranged step attends over the fresh rows only",
+     "return xo_attention(q, kv_buf, kv_buf + plane, B, Nq, N, H, d, rows, nrows, out, lse);",
+     "return xo_attention(q, fresh_k, fresh_v, B, Nq, F, H, d, rows, nrows, out, lse);"),
 ]
 
 
