@@ -45,6 +45,9 @@ enum { XDIT_BF16 = 0, XDIT_F32 = 1 };
 /* Upper bound on the number of partials one xdit_lse_merge call accepts. */
 #define XDIT_MAX_PARTIALS 64
 
+/* Upper bound on the fresh row ranges of one xdit_patch_attn_ranges call. */
+#define XDIT_MAX_RANGES 2
+
 typedef enum {
     XDIT_OK = 0,
     XDIT_ERR_NULL = -1,        /* a required pointer is NULL                  */
@@ -84,6 +87,39 @@ int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patc
                     const void* fresh_k, const void* fresh_v, void* out,
                     int64_t batch, int64_t seq_len, int64_t heads, int64_t head_dim,
                     int32_t dtype);
+
+/*
+ * The patch step in its general form (Sections 4.1.2 and 4.1.4): the fresh
+ * K/V rows cover up to XDIT_MAX_RANGES disjoint row ranges of the buffer and
+ * the queries are rows of their own.  Two uses come from the paper:
+ *   - in-context conditioning (Section 4.1.2): the text tokens travel with
+ *     patch 0, so that micro-step refreshes the patch's image rows and the
+ *     text rows, and its queries are the rows of both;
+ *   - hybrid parallelism (Section 4.1.4): a PipeFusion stage stores the K/V
+ *     gathered over its sequence-parallel group while its queries are only
+ *     the local shard, so every rank's buffer stays identical.
+ * First rows [range_off[r], range_off[r] + range_len[r]) of both planes are
+ * overwritten with the fresh rows (range 0's rows first, then range 1's),
+ * then out = attention(q, updated K, updated V) and, if lse is not NULL, its
+ * log-sum-exp.  xdit_patch_attn is the case of one range with q_len equal to
+ * its length and no LSE.
+ *
+ *   q          [B, q_len, H, d]
+ *   kv_buf     [2, B, seq_len, H, d]  MUTATED as above
+ *   n_ranges   0 .. XDIT_MAX_RANGES; range_off / range_len are HOST arrays of
+ *              n_ranges entries, each range inside [0, seq_len), pairwise
+ *              disjoint (empty ranges allowed)
+ *   fresh_k, fresh_v [B, F, H, d], F = sum of range_len
+ *   out        [B, q_len, H, d]
+ *   lse        [B, H, q_len] float32, or NULL
+ * q_len = 0 performs only the update; F = 0 is plain attention over the
+ * buffer.  out and lse must not overlap any input or each other; the fresh
+ * rows must not overlap kv_buf.
+ */
+int xdit_patch_attn_ranges(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
+                           const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
+                           const void* fresh_v, void* out, float* lse, int64_t batch,
+                           int64_t seq_len, int64_t heads, int64_t head_dim, int32_t dtype);
 
 /*
  * Sequence-parallel chunk step (Section 4.1.1: SP-Ring computes attention as

@@ -13,10 +13,12 @@ from __future__ import annotations
 
 import ctypes
 
-from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XditError, check, lib)
+from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XditError, check,
+                   lib)
 
-__all__ = ["xdit_patch_attn", "xdit_chunk_attn", "xdit_lse_merge", "xdit_kv_update",
-           "set_stream", "XditError", "XDIT_MAX_PARTIALS", "version"]
+__all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn", "xdit_lse_merge",
+           "xdit_kv_update", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
+           "version"]
 
 
 def _torch():
@@ -82,6 +84,37 @@ def xdit_patch_attn(q, kv_buf, patch_off: int, patch_len: int, fresh_k, fresh_v,
     check(lib().xdit_patch_attn(_ptr(q), _ptr(kv_buf), int(patch_off), int(patch_len),
                                 _ptr(fresh_k), _ptr(fresh_v), _ptr(out), B, N, H, d,
                                 _dtype_code(kv_buf)))
+
+
+def xdit_patch_attn_ranges(q, kv_buf, ranges, fresh_k, fresh_v, out, lse=None) -> None:
+    """General patch step: write fresh_k/fresh_v [B, F, H, d] into the row
+    ranges [(off, len), ...] of kv_buf [2,B,N,H,d] (range 0's rows first; F =
+    sum of the lengths), then out = attention(q, updated K, updated V) for the
+    queries q [B,Nq,H,d] and, if given, lse [B,H,Nq] (natural log)."""
+    _dense(kv_buf, "kv_buf", 5)
+    for t, n in ((q, "q"), (fresh_k, "fresh_k"), (fresh_v, "fresh_v"), (out, "out")):
+        _dense(t, n, 4)
+    _dense(lse, "lse", 3)
+    _, B, N, H, d = kv_buf.shape
+    nr = len(ranges)
+    F = sum(int(r[1]) for r in ranges)
+    Nq = q.shape[1]
+    for t, n, rows in ((q, "q", Nq), (out, "out", Nq), (fresh_k, "fresh_k", F),
+                       (fresh_v, "fresh_v", F)):
+        if tuple(t.shape) != (B, rows, H, d):
+            raise XditError(-3, f"{n} has shape {tuple(t.shape)}, expected {(B, rows, H, d)}")
+        if t.dtype != kv_buf.dtype:
+            raise XditError(-2, f"{n} dtype {t.dtype} differs from kv_buf's {kv_buf.dtype}")
+    if lse is not None:
+        torch = _torch()
+        if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, Nq):
+            raise XditError(-3, f"lse must be float32 [B,H,Nq] = {(B, H, Nq)}")
+    offs = (ctypes.c_int64 * max(nr, 1))(*[int(r[0]) for r in ranges])
+    lens = (ctypes.c_int64 * max(nr, 1))(*[int(r[1]) for r in ranges])
+    _use_current_stream()
+    check(lib().xdit_patch_attn_ranges(_ptr(q), Nq, _ptr(kv_buf), nr, offs, lens, _ptr(fresh_k),
+                                       _ptr(fresh_v), _ptr(out), _ptr(lse), B, N, H, d,
+                                       _dtype_code(kv_buf)))
 
 
 def xdit_chunk_attn(q, k, v, out, lse=None) -> None:

@@ -21,6 +21,7 @@ STATUS = {
 }
 XDIT_BF16, XDIT_F32 = 0, 1
 XDIT_MAX_PARTIALS = 64
+XDIT_MAX_RANGES = 2
 
 _vp = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -29,6 +30,8 @@ _i32 = ctypes.c_int32
 SIGNATURES = {
     "xdit_patch_attn": (ctypes.c_int, [_vp, _vp, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _i64, _i64,
                                        _i32]),
+    "xdit_patch_attn_ranges": (ctypes.c_int, [_vp, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                              _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
     "xdit_lse_merge": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_kv_update": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),

@@ -122,7 +122,8 @@ struct Args {
     uint16_t* wv;
     uint16_t* out;
     float* lse;
-    int B, H, Nq, Nk, off, len, q_tiles;
+    int B, H, Nq, Nk, q_tiles;
+    int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
     float c2;  // softmax scale * log2(e)
 };
 
@@ -231,8 +232,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const int64_t headoff = (int64_t)hh * D;
     const uint16_t* kbase = a.k + (int64_t)b * a.Nk * a.H * D + headoff;
     const uint16_t* vbase = a.v + (int64_t)b * a.Nk * a.H * D + headoff;
-    const uint16_t* fkbase = PATCH ? a.fk + (int64_t)b * a.len * a.H * D + headoff : nullptr;
-    const uint16_t* fvbase = PATCH ? a.fv + (int64_t)b * a.len * a.H * D + headoff : nullptr;
+    const int F = a.len0 + a.len1;  // fresh rows
+    const uint16_t* fkbase = PATCH ? a.fk + (int64_t)b * F * a.H * D + headoff : nullptr;
+    const uint16_t* fvbase = PATCH ? a.fv + (int64_t)b * F * a.H * D + headoff : nullptr;
     auto rows_rsrc = [&](const uint16_t* base, int row0, int rows) -> Rsrc {
         return rsrc(base + (int64_t)row0 * a.H * D, (uint32_t)(rows - row0) * rowb - headb);
     };
@@ -261,32 +263,39 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
         qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
     }
-    // Patch mode: this workgroup's share of the fresh slice goes into the
+    // Patch mode: this workgroup's share of the fresh rows goes into the
     // buffer (all query tiles of a (batch, head) split the rows).  Nobody
-    // reads the slice rows of the buffer: they are taken from the fresh rows.
+    // reads the fresh ranges of the buffer: they are taken from the fresh
+    // rows.
     if constexpr (PATCH) {
-        const int r0 = (int)((int64_t)a.len * qt / a.q_tiles);
-        const int r1 = (int)((int64_t)a.len * (qt + 1) / a.q_tiles);
-        const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
-        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), a.off, a.Nk);
-        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), a.off, a.Nk);
-        // a workgroup's share is at most BM rows (q_tiles = ceil(len / BM)):
-        // all loads first, then all stores; chunks past the share use the
-        // out-of-range offset (reads give zero, writes are dropped)
-        constexpr int U = (C::BM * C::CH + NT - 1) / NT;
-        uint32_t co[U];
-        u32x4 ck[U], cv[U];
+        const int r0 = (int)((int64_t)F * qt / a.q_tiles);
+        const int r1 = (int)((int64_t)F * (qt + 1) / a.q_tiles);
+        const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
+        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), 0, a.Nk);
+        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), 0, a.Nk);
+        // batches of U chunks per lane: all loads first, then all stores;
+        // chunks past the share use the out-of-range offset (reads give
+        // zero, writes are dropped)
+        constexpr int U = 4;
+        const int nchunks = (r1 - r0) * C::CH;
+        for (int e0 = 0; e0 < nchunks; e0 += U * NT) {
+            uint32_t cs[U], cd[U];
+            u32x4 ck[U], cv[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int e = tid + u * NT;
-            co[u] = e < (r1 - r0) * C::CH ? (uint32_t)(r0 + e / C::CH) * rowb + 16 * (e % C::CH) : kOOB;
-            ck[u] = bload(fk, co[u]);
-            cv[u] = bload(fv, co[u]);
-        }
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + tid + u * NT;
+                const int fr = r0 + e / C::CH, cc = 16 * (e % C::CH);
+                const int j = fr < a.len0 ? a.off0 + fr : a.off1 + fr - a.len0;  // buffer row
+                cs[u] = e < nchunks ? (uint32_t)fr * rowb + cc : kOOB;
+                cd[u] = e < nchunks ? (uint32_t)j * rowb + cc : kOOB;
+                ck[u] = bload(fk, cs[u]);
+                cv[u] = bload(fv, cs[u]);
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            bstore(wk, co[u], ck[u]);
-            bstore(wv, co[u], cv[u]);
+            for (int u = 0; u < U; ++u) {
+                bstore(wk, cd[u], ck[u]);
+                bstore(wv, cd[u], cv[u]);
+            }
         }
         // no wait: the stores are older than every tile load, and vector
         // memory operations of a wave complete in issue order, so the first
@@ -307,15 +316,17 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         dma_off[n] = (uint32_t)r * rowb + 16 * (pc ^ (r & C::SWZ_MASK));
     }
 
-    auto in_slice = [&](int j) -> bool { return (unsigned)(j - a.off) < (unsigned)a.len; };
     // Where a tile's rows come from (uniform across the workgroup): all from
-    // the buffer (or the chunk), all from the fresh rows, or both.
-    enum { kBuf = 0, kFresh = 1, kMixed = 2 };
+    // the buffer (or the chunk), all from one fresh range, or several sources.
+    enum { kBuf = 0, kFresh0 = 1, kFresh1 = 2, kMixed = 3 };
     auto tile_kind = [&](int t) -> int {
         if constexpr (!PATCH) return kBuf;
         const int lo = t * BN, hi = min(lo + BN, a.Nk);
-        if (hi <= a.off || lo >= a.off + a.len) return kBuf;
-        if (a.off <= lo && hi <= a.off + a.len) return kFresh;
+        const bool x0 = a.len0 > 0 && lo < a.off0 + a.len0 && a.off0 < hi;
+        const bool x1 = a.len1 > 0 && lo < a.off1 + a.len1 && a.off1 < hi;
+        if (!x0 && !x1) return kBuf;
+        if (!x1 && a.off0 <= lo && hi <= a.off0 + a.len0) return kFresh0;
+        if (!x0 && a.off1 <= lo && hi <= a.off1 + a.len1) return kFresh1;
         return kMixed;
     };
 
@@ -325,8 +336,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         unsigned char* kdst = stage(s);
         unsigned char* vdst = stage(s) + C::TILE_BYTES;
         if (kind != kMixed) {
-            const Rsrc rk = kind == kBuf ? rows_rsrc(kbase, lo, a.Nk) : rows_rsrc(fkbase, lo - a.off, a.len);
-            const Rsrc rv = kind == kBuf ? rows_rsrc(vbase, lo, a.Nk) : rows_rsrc(fvbase, lo - a.off, a.len);
+            // fresh row of buffer row j: j - off0 in range 0, len0 + j - off1
+            // in range 1; each range's resource ends at its last fresh row
+            const int fbase = kind == kFresh0 ? -a.off0 : a.len0 - a.off1;
+            const int fend = kind == kFresh0 ? a.len0 : F;
+            const Rsrc rk = kind == kBuf ? rows_rsrc(kbase, lo, a.Nk) : rows_rsrc(fkbase, lo + fbase, fend);
+            const Rsrc rv = kind == kBuf ? rows_rsrc(vbase, lo, a.Nk) : rows_rsrc(fvbase, lo + fbase, fend);
 #pragma unroll
             for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
                 const int ins = wave + n * C::NW;
@@ -336,18 +351,22 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 }
             }
         } else {
-            // the tile straddles a slice boundary (at most two per sweep):
+            // the tile straddles a range boundary (at most four per sweep):
             // each lane loads its row from its own source
             const Rsrc rk = rows_rsrc(kbase, lo, a.Nk), rv = rows_rsrc(vbase, lo, a.Nk);
-            const Rsrc fk = rows_rsrc(fkbase, 0, a.len), fv = rows_rsrc(fvbase, 0, a.len);
-            const uint32_t shift = (uint32_t)(lo - a.off) * rowb;  // fresh row = tile row + lo - off
+            const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
 #pragma unroll
             for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
                 const int ins = wave + n * C::NW;
                 if (C::DMA_PER_TILE % C::NW == 0 || ins < C::DMA_PER_TILE) {
-                    if (in_slice(lo + dma_row[n])) {
-                        dma16(fk, kdst + 1024 * ins, dma_off[n] + shift);
-                        dma16(fv, vdst + 1024 * ins, dma_off[n] + shift);
+                    const int j = lo + dma_row[n];
+                    const bool in0 = (unsigned)(j - a.off0) < (unsigned)a.len0;
+                    const bool in1 = (unsigned)(j - a.off1) < (unsigned)a.len1;
+                    if (in0 || in1) {
+                        const int fr = in0 ? j - a.off0 : a.len0 + j - a.off1;
+                        const uint32_t o = dma_off[n] + (uint32_t)(fr - dma_row[n]) * rowb;
+                        dma16(fk, kdst + 1024 * ins, o);
+                        dma16(fv, vdst + 1024 * ins, o);
                     } else {
                         dma16(rk, kdst + 1024 * ins, dma_off[n]);
                         dma16(rv, vdst + 1024 * ins, dma_off[n]);
@@ -677,8 +696,10 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.H = p.H;
     a.Nq = p.Nq;
     a.Nk = p.Nk;
-    a.off = p.off;
-    a.len = p.len;
+    a.off0 = p.off0;
+    a.len0 = p.len0;
+    a.off1 = p.off1;
+    a.len1 = p.len1;
     a.q_tiles = (p.Nq + C::BM - 1) / C::BM;
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;

@@ -28,7 +28,8 @@ struct Args {
     float* wv;
     float* out;
     float* lse;
-    int B, H, Nq, Nk, off, len, q_tiles;
+    int B, H, Nq, Nk, q_tiles;
+    int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
     float scale;
 };
 
@@ -65,8 +66,13 @@ __global__ __launch_bounds__(kFBM) void attn_f32_kernel(Args a) {
     }
     float m = -INFINITY, l = 0.f;
 
-    auto in_slice = [&](int j) -> bool {
-        return PATCH && (unsigned)(j - a.off) < (unsigned)a.len;
+    // row of the fresh tensors that holds buffer row j, or -1
+    const int F = a.len0 + a.len1;
+    auto fresh_row = [&](int j) -> int {
+        if (!PATCH) return -1;
+        if ((unsigned)(j - a.off0) < (unsigned)a.len0) return j - a.off0;
+        if ((unsigned)(j - a.off1) < (unsigned)a.len1) return a.len0 + j - a.off1;
+        return -1;
     };
 
     const int ntiles = (a.Nk + kFBN - 1) / kFBN;
@@ -77,8 +83,9 @@ __global__ __launch_bounds__(kFBM) void attn_f32_kernel(Args a) {
             f32x4 kx = {0.f, 0.f, 0.f, 0.f}, vx = {0.f, 0.f, 0.f, 0.f};
             if (j < a.Nk) {
                 const float *kp, *vp;
-                if (in_slice(j)) {
-                    const int64_t o2 = ((int64_t)b * a.len + (j - a.off)) * rs + (int64_t)hh * D + 4 * cc;
+                const int fr = fresh_row(j);
+                if (fr >= 0) {
+                    const int64_t o2 = ((int64_t)b * F + fr) * rs + (int64_t)hh * D + 4 * cc;
                     kp = a.fk + o2;
                     vp = a.fv + o2;
                 } else {
@@ -88,7 +95,7 @@ __global__ __launch_bounds__(kFBM) void attn_f32_kernel(Args a) {
                 }
                 kx = *(const f32x4*)kp;
                 vx = *(const f32x4*)vp;
-                if (writeback && in_slice(j)) {
+                if (writeback && fr >= 0) {
                     const int64_t o3 = ((int64_t)b * a.Nk + j) * rs + (int64_t)hh * D + 4 * cc;
                     *(f32x4*)(a.wk + o3) = kx;
                     *(f32x4*)(a.wv + o3) = vx;
@@ -150,8 +157,10 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.H = p.H;
     a.Nq = p.Nq;
     a.Nk = p.Nk;
-    a.off = p.off;
-    a.len = p.len;
+    a.off0 = p.off0;
+    a.len0 = p.len0;
+    a.off1 = p.off1;
+    a.len1 = p.len1;
     a.q_tiles = (p.Nq + kFBM - 1) / kFBM;
     a.scale = (float)(1.0 / sqrt((double)D));
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;

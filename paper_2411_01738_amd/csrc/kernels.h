@@ -8,20 +8,22 @@
 namespace xdit {
 
 // One attention launch: chunk attention (fresh_k == nullptr) or a fused
-// PipeFusion patch step (K/V rows [off, off+len) come from fresh_k/fresh_v and
-// are written back into the buffer planes wk/wv).
+// PipeFusion patch step: K/V rows in the fresh ranges [off0, off0+len0) and
+// [off1, off1+len1) come from fresh_k/fresh_v (rows 0..len0-1, then
+// len0..len0+len1-1) and are written back into the buffer planes wk/wv.
 struct AttnParams {
     const void* q;        // [B, Nq, H, D]
     const void* k;        // [B, Nk, H, D]  (patch: K plane of the buffer)
     const void* v;        // [B, Nk, H, D]  (patch: V plane of the buffer)
-    const void* fresh_k;  // [B, len, H, D] or nullptr
+    const void* fresh_k;  // [B, len0 + len1, H, D] or nullptr
     const void* fresh_v;
     void* wk;             // patch write-back target planes (== k / v) or nullptr
     void* wv;
     void* out;            // [B, Nq, H, D]
     float* lse;           // [B, H, Nq] or nullptr
     int B, H, Nq, Nk, D;
-    int off, len;         // patch slice; len == 0 for chunk attention
+    int off0, len0;       // first fresh range
+    int off1, len1;       // second fresh range (len1 == 0: none); disjoint from the first
 };
 
 struct MergeParams {
@@ -33,11 +35,14 @@ struct MergeParams {
     int B, Nq, H, D;
 };
 
+// Copy fresh rows [fbase, fbase+len) of fresh_k/fresh_v [B, frows, H, D]
+// into rows [off, off+len) of both buffer planes.
 struct UpdateParams {
     void* kv_buf;             // [2, B, N, H, D]
-    const void* fresh_k;      // [B, len, H, D]
+    const void* fresh_k;      // [B, frows, H, D]
     const void* fresh_v;
     int B, N, H, D, off, len;
+    int frows, fbase;
     int esize;                // bytes per element
 };
 

@@ -116,19 +116,20 @@ hipError_t launch_merge(const MergeParams& p, hipStream_t s) {
 
 struct UpdateArgs {
     u32x4* kv;            // buffer base
-    const u32x4* fk;
+    const u32x4* fk;      // fresh rows, already offset to row fbase of batch 0
     const u32x4* fv;
     int64_t plane_vecs;   // B * N * H * D * esize / 16
     int64_t batch_vecs;   // N * H * D * esize / 16
     int64_t off_vecs;     // off * H * D * esize / 16
     int64_t slice_vecs;   // len * H * D * esize / 16 (per batch)
+    int64_t fbatch_vecs;  // frows * H * D * esize / 16
     int B;
 };
 
 // blockIdx.y = plane * B + b; the slice of one (plane, batch) is contiguous.
 __global__ __launch_bounds__(kThreads) void kv_update_kernel(UpdateArgs a) {
     const int plane = blockIdx.y / a.B, b = blockIdx.y % a.B;
-    const u32x4* src = (plane ? a.fv : a.fk) + (int64_t)b * a.slice_vecs;
+    const u32x4* src = (plane ? a.fv : a.fk) + (int64_t)b * a.fbatch_vecs;
     u32x4* dst = a.kv + plane * a.plane_vecs + (int64_t)b * a.batch_vecs + a.off_vecs;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x; v < a.slice_vecs; v += stride)
@@ -144,8 +145,9 @@ hipError_t launch_kv_update(const UpdateParams& p, hipStream_t s) {
     const int64_t row_vecs = (int64_t)p.H * p.D * p.esize / 16;
     UpdateArgs a;
     a.kv = (u32x4*)p.kv_buf;
-    a.fk = (const u32x4*)p.fresh_k;
-    a.fv = (const u32x4*)p.fresh_v;
+    a.fk = (const u32x4*)p.fresh_k + (int64_t)p.fbase * row_vecs;
+    a.fv = (const u32x4*)p.fresh_v + (int64_t)p.fbase * row_vecs;
+    a.fbatch_vecs = (int64_t)p.frows * row_vecs;
     a.batch_vecs = (int64_t)p.N * row_vecs;
     a.plane_vecs = (int64_t)p.B * a.batch_vecs;
     a.off_vecs = (int64_t)p.off * row_vecs;

@@ -169,6 +169,101 @@ static int check_patch_args(const char* fn, const void* q, void* kv_buf, int64_t
     return XDIT_OK;
 }
 
+// The patch step in its general form: fresh rows over up to
+// XDIT_MAX_RANGES disjoint row ranges, queries of their own.
+static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void* kv_buf,
+                             int32_t n_ranges, const int64_t* range_off, const int64_t* range_len,
+                             const void* fresh_k, const void* fresh_v, void* out, float* lse,
+                             int64_t batch, int64_t seq_len, int64_t heads, int64_t head_dim,
+                             int32_t dtype) {
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    if (n_ranges < 0 || n_ranges > XDIT_MAX_RANGES)
+        return fail(XDIT_ERR_RANGE, "%s: n_ranges = %d outside [0, %d]", fn, n_ranges, XDIT_MAX_RANGES);
+    if (n_ranges > 0 && (range_off == nullptr || range_len == nullptr))
+        return fail(XDIT_ERR_NULL, "%s: range_off / range_len host arrays are NULL", fn);
+    XDIT_TRY(check_dims(fn, batch, seq_len, q_len, heads));
+    int64_t off[XDIT_MAX_RANGES] = {0, 0}, len[XDIT_MAX_RANGES] = {0, 0};
+    int64_t F = 0;
+    for (int r = 0; r < n_ranges; ++r) {
+        off[r] = range_off[r];
+        len[r] = range_len[r];
+        if (off[r] < 0 || len[r] < 0 || off[r] > seq_len - len[r])
+            return fail(XDIT_ERR_RANGE, "%s: range %d [%lld, %lld) outside the buffer of %lld rows", fn, r,
+                        (long long)off[r], (long long)(off[r] + len[r]), (long long)seq_len);
+        for (int r2 = 0; r2 < r; ++r2)
+            if (len[r] > 0 && len[r2] > 0 && off[r] < off[r2] + len[r2] && off[r2] < off[r] + len[r])
+                return fail(XDIT_ERR_RANGE, "%s: ranges %d and %d overlap", fn, r2, r);
+        F += len[r];
+    }
+    const int es = esize_of(dtype);
+    int64_t most = seq_len > q_len ? seq_len : q_len;
+    XDIT_TRY(check_batch_bytes(fn, most, heads, head_dim, es));
+    const int64_t row = heads * head_dim * es;
+    const Span sb{kv_buf, 2 * batch * seq_len * row, "kv_buf"}, sk{fresh_k, batch * F * row, "fresh_k"},
+        sv{fresh_v, batch * F * row, "fresh_v"}, sq{q, batch * q_len * row, "q"},
+        so{out, batch * q_len * row, "out"}, sl{lse, lse ? batch * heads * q_len * 4 : 0, "lse"};
+    for (const Span* s : {&sb, &sk, &sv, &sq, &so}) XDIT_TRY(check_ptr(*s));
+    if (lse && ((uintptr_t)lse & 3u)) return fail(XDIT_ERR_LAYOUT, "lse is not 4-byte aligned");
+    XDIT_TRY(check_no_overlap(sk, sb));
+    XDIT_TRY(check_no_overlap(sv, sb));
+    for (const Span* s : {&sq, &sb, &sk, &sv}) {
+        XDIT_TRY(check_no_overlap(so, *s));
+        XDIT_TRY(check_no_overlap(sl, *s));
+    }
+    XDIT_TRY(check_no_overlap(sl, so));
+    if (batch == 0 || heads == 0) return XDIT_OK;
+
+    const int64_t plane = batch * seq_len * row;
+    if (q_len == 0) {
+        // no queries: only the update
+        int64_t base = 0;
+        for (int r = 0; r < n_ranges; ++r) {
+            if (len[r] > 0) {
+                xdit::UpdateParams u{};
+                u.kv_buf = kv_buf;
+                u.fresh_k = fresh_k;
+                u.fresh_v = fresh_v;
+                u.B = (int)batch;
+                u.N = (int)seq_len;
+                u.H = (int)heads;
+                u.D = (int)head_dim;
+                u.off = (int)off[r];
+                u.len = (int)len[r];
+                u.frows = (int)F;
+                u.fbase = (int)base;
+                u.esize = es;
+                XDIT_TRY(hip_status(xdit::launch_kv_update(u, g_stream), fn));
+            }
+            base += len[r];
+        }
+        return XDIT_OK;
+    }
+    xdit::AttnParams p{};
+    p.q = q;
+    p.k = kv_buf;
+    p.v = (const char*)kv_buf + plane;
+    if (F > 0) {
+        p.fresh_k = fresh_k;
+        p.fresh_v = fresh_v;
+        p.wk = kv_buf;
+        p.wv = (char*)kv_buf + plane;
+    }
+    p.out = out;
+    p.lse = lse;
+    p.B = (int)batch;
+    p.H = (int)heads;
+    p.Nq = (int)q_len;
+    p.Nk = (int)seq_len;
+    p.D = (int)head_dim;
+    p.off0 = (int)off[0];
+    p.len0 = (int)len[0];
+    p.off1 = (int)off[1];
+    p.len1 = (int)len[1];
+    const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
+                                            : xdit::launch_attn_f32(p, g_stream);
+    return hip_status(e, fn);
+}
+
 int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patch_len,
                     const void* fresh_k, const void* fresh_v, void* out, int64_t batch,
                     int64_t seq_len, int64_t heads, int64_t head_dim, int32_t dtype) {
@@ -178,28 +273,18 @@ int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patc
     XDIT_TRY(check_patch_args("xdit_patch_attn", q, kv_buf, patch_off, patch_len, fresh_k,
                               fresh_v, out, batch, seq_len, heads, head_dim, dtype));
     if (batch == 0 || patch_len == 0 || heads == 0) return XDIT_OK;
+    return patch_ranges_impl("xdit_patch_attn", q, patch_len, kv_buf, 1, &patch_off, &patch_len,
+                             fresh_k, fresh_v, out, nullptr, batch, seq_len, heads, head_dim, dtype);
+}
 
-    const int64_t plane = batch * seq_len * heads * head_dim * esize_of(dtype);
-    xdit::AttnParams p{};
-    p.q = q;
-    p.k = kv_buf;
-    p.v = (const char*)kv_buf + plane;
-    p.fresh_k = fresh_k;
-    p.fresh_v = fresh_v;
-    p.wk = kv_buf;
-    p.wv = (char*)kv_buf + plane;
-    p.out = out;
-    p.lse = nullptr;
-    p.B = (int)batch;
-    p.H = (int)heads;
-    p.Nq = (int)patch_len;
-    p.Nk = (int)seq_len;
-    p.D = (int)head_dim;
-    p.off = (int)patch_off;
-    p.len = (int)patch_len;
-    const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
-                                            : xdit::launch_attn_f32(p, g_stream);
-    return hip_status(e, "xdit_patch_attn launch");
+int xdit_patch_attn_ranges(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
+                           const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
+                           const void* fresh_v, void* out, float* lse, int64_t batch,
+                           int64_t seq_len, int64_t heads, int64_t head_dim, int32_t dtype) {
+    clear_error();
+    return patch_ranges_impl("xdit_patch_attn_ranges", q, q_len, kv_buf, n_ranges, range_off,
+                             range_len, fresh_k, fresh_v, out, lse, batch, seq_len, heads, head_dim,
+                             dtype);
 }
 
 int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const void* fresh_k,
@@ -219,6 +304,8 @@ int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const voi
     p.D = (int)head_dim;
     p.off = (int)patch_off;
     p.len = (int)patch_len;
+    p.frows = (int)patch_len;
+    p.fbase = 0;
     p.esize = esize_of(dtype);
     return hip_status(xdit::launch_kv_update(p, g_stream), "xdit_kv_update launch");
 }

@@ -27,8 +27,9 @@ def header_functions():
 
 def test_header_declares_the_entry_points():
     names = header_functions()
-    for fn in ["xdit_patch_attn", "xdit_chunk_attn", "xdit_lse_merge", "xdit_kv_update",
-               "xdit_set_stream", "xdit_get_stream", "xdit_last_error", "xdit_version"]:
+    for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn", "xdit_lse_merge",
+               "xdit_kv_update", "xdit_set_stream", "xdit_get_stream", "xdit_last_error",
+               "xdit_version"]:
         assert fn in names
 
 
@@ -116,12 +117,51 @@ def test_merge_rejections():
     assert lib.xdit_lse_merge(outs, lses, 2, P(5), None, 1, 16, 2, 96, 0) == -7
 
 
+def _ranges(*rs):
+    offs = (ctypes.c_int64 * max(len(rs), 1))(*[r[0] for r in rs])
+    lens = (ctypes.c_int64 * max(len(rs), 1))(*[r[1] for r in rs])
+    return len(rs), offs, lens
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("ranges,q_len,fk,out,lse,code", [
+    ([(0, 4), (8, 4), (12, 2)], 8, P(2), P(4), P(5), -4),    # more than XDIT_MAX_RANGES
+    ([(0, 6), (4, 4)], 8, P(2), P(4), P(5), -4),             # overlapping ranges
+    ([(0, 4), (14, 4)], 8, P(2), P(4), P(5), -4),            # past the end of the buffer
+    ([(-1, 4)], 8, P(2), P(4), P(5), -4),                    # negative offset
+    ([(0, 4)], -1, P(2), P(4), P(5), -3),                    # negative q_len
+    ([(0, 4)], 8, P(1) + 512, P(4), P(5), -6),               # fresh rows inside kv_buf
+    ([(0, 4)], 8, P(2), P(4), P(4) + 64, -6),                # lse inside out
+    ([(0, 4)], 8, P(2), P(4), P(5) + 2, -5),                 # lse misaligned
+    ([(0, 4)], 8, P(2), P(1), P(5), -6),                     # out inside kv_buf
+    ([(0, 4)], 8, None, P(4), P(5), -1),                     # fresh rows missing
+])
+def test_ranges_rejections(ranges, q_len, fk, out, lse, code):
+    lib = _lib.lib()
+    n, offs, lens = _ranges(*ranges)
+    assert lib.xdit_patch_attn_ranges(P(0), q_len, P(1), n, offs, lens, fk, P(3), out, lse,
+                                      1, 16, 2, 64, 0) == code
+    assert lib.xdit_last_error().decode(), "no message for a rejected call"
+
+
+@needs_no_gpu
+def test_ranges_rejects_null_range_arrays():
+    lib = _lib.lib()
+    assert lib.xdit_patch_attn_ranges(P(0), 8, P(1), 1, None, None, P(2), P(3), P(4), None,
+                                      1, 16, 2, 64, 0) == -1
+
+
 @needs_no_gpu
 def test_empty_calls_succeed_without_launching():
     lib = _lib.lib()
     assert lib.xdit_chunk_attn(None, None, None, None, None, 1, 0, 0, 2, 64, 0) == 0
     assert lib.xdit_patch_attn(None, P(1), 16, 0, None, None, None, 1, 16, 2, 64, 0) == 0
     assert lib.xdit_kv_update(P(1), 3, 0, None, None, 1, 16, 2, 128, 1) == 0
+    n, offs, lens = _ranges((3, 0), (9, 0))
+    assert lib.xdit_patch_attn_ranges(None, 0, P(1), n, offs, lens, None, None, None, None,
+                                      1, 16, 2, 64, 0) == 0
+    assert lib.xdit_patch_attn_ranges(P(0), 8, P(1), 1, offs, lens, None, None, P(4), None,
+                                      0, 16, 2, 64, 0) == 0
     assert lib.xdit_last_error().decode() == ""
 
 

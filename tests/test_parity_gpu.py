@@ -295,3 +295,135 @@ def test_patch_all_fresh_equals_chunk_attention(torch):
         xd.xdit_chunk_attn(q, k, v, o2, None)
         torch.cuda.synchronize()
         assert torch.equal(o1, o2)
+
+
+# ---------------------------------------------------------------------------
+# General patch step: several fresh ranges, queries of their own
+# ---------------------------------------------------------------------------
+RANGE_CASES = [
+    # dtype, B, N, H, d, fresh ranges
+    ("bf16", 2, 300, 2, 64, [(0, 80), (240, 60)]),     # patch 0 + the text rows after the image
+    ("bf16", 1, 400, 2, 72, [(100, 60), (250, 50)]),   # both ranges straddle 128-row tiles
+    ("bf16", 1, 333, 2, 128, [(0, 200), (300, 33)]),
+    ("bf16", 1, 520, 2, 64, [(384, 136), (0, 256)]),   # range order differs from row order
+    ("f32", 1, 200, 2, 64, [(10, 50), (150, 50)]),
+    ("f32", 2, 150, 2, 72, [(0, 40), (120, 30)]),
+    ("f32", 1, 97, 2, 128, [(0, 32), (64, 33)]),
+]
+
+
+def _range_rows(ranges):
+    return np.concatenate([np.arange(o, o + n) for o, n in ranges]).astype(np.int64)
+
+
+@pytest.mark.parametrize("dtype,B,N,H,d,ranges", RANGE_CASES)
+def test_patch_ranges_in_context(orc, torch, tile_shape, dtype, B, N, H, d, ranges):
+    """Patch 0 carrying the text rows: the queries are the rows of both
+    ranges; then the remaining image patches run as single-range steps."""
+    seed = 8000 + N + d
+    q = random_io((B, N, H, d), dtype, seed)
+    kf = random_io((B, N, H, d), dtype, seed + 1)
+    vf = random_io((B, N, H, d), dtype, seed + 2)
+    kv_ref = np.ascontiguousarray(np.stack([random_io((B, N, H, d), dtype, seed + 3),
+                                            random_io((B, N, H, d), dtype, seed + 4)]))
+    kv = to_gpu(kv_ref, dtype)
+    rows = _range_rows(ranges)
+    qs, fks, fvs = q[:, rows].copy(), kf[:, rows].copy(), vf[:, rows].copy()
+    ref_o, ref_l = orc.patch_ranges(qs, kv_ref, ranges, fks, fvs)
+    out = _empty_out(torch, B, len(rows), H, d, dtype)
+    lse = torch.full((B, H, len(rows)), float("nan"), device="cuda", dtype=torch.float32)
+    xd.xdit_patch_attn_ranges(to_gpu(qs, dtype), kv, ranges, to_gpu(fks, dtype),
+                              to_gpu(fvs, dtype), out, lse)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, dtype, f"ranges {ranges} out")
+    check_lse(lse.cpu().numpy(), ref_l, dtype, f"ranges {ranges} lse")
+    assert np.array_equal(to_np(kv), kv_ref), f"ranges {ranges}: buffer not bit-exact"
+    # a later single-range step sees the fresh text rows
+    off, ln = ranges[0][0] + ranges[0][1], 40
+    if off + ln <= N and not any(o < off + ln and off < o + n for o, n in ranges):
+        sl = slice(off, off + ln)
+        ref_o2, _ = orc.patch(q[:, sl].copy(), kv_ref, off, kf[:, sl].copy(), vf[:, sl].copy())
+        out2 = _empty_out(torch, B, ln, H, d, dtype)
+        xd.xdit_patch_attn(to_gpu(q[:, sl], dtype), kv, off, ln, to_gpu(kf[:, sl], dtype),
+                           to_gpu(vf[:, sl], dtype), out2)
+        torch.cuda.synchronize()
+        check_out(to_np(out2), ref_o2, dtype, "step after the in-context patch")
+        assert np.array_equal(to_np(kv), kv_ref)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 72), ("bf16", 128), ("f32", 72)])
+def test_patch_ranges_sp_shards(orc, torch, tile_shape, dtype, d):
+    """Hybrid SP x PipeFusion at one GPU's share: each of sp ranks stores the
+    same gathered fresh K/V and attends with its own query shard; the buffers
+    end identical and the shards' outputs assemble the unsharded step."""
+    B, N, H, off, ln, sp = 1, 384, 2, 96, 192, 4
+    seed = 9000 + d
+    q = random_io((B, ln, H, d), dtype, seed)
+    fk = random_io((B, ln, H, d), dtype, seed + 1)
+    fv = random_io((B, ln, H, d), dtype, seed + 2)
+    kv0 = np.ascontiguousarray(np.stack([random_io((B, N, H, d), dtype, seed + 3),
+                                         random_io((B, N, H, d), dtype, seed + 4)]))
+    kv_ref = kv0.copy()
+    ref_o, ref_l = orc.patch_ranges(q, kv_ref, [(off, ln)], fk, fv)
+    outs, lses, bufs = [], [], []
+    for r in range(sp):
+        sh = slice(r * ln // sp, (r + 1) * ln // sp)
+        kv = to_gpu(kv0, dtype)
+        n = sh.stop - sh.start
+        out = _empty_out(torch, B, n, H, d, dtype)
+        lse = torch.empty((B, H, n), device="cuda", dtype=torch.float32)
+        xd.xdit_patch_attn_ranges(to_gpu(q[:, sh], dtype), kv, [(off, ln)], to_gpu(fk, dtype),
+                                  to_gpu(fv, dtype), out, lse)
+        torch.cuda.synchronize()
+        outs.append(to_np(out))
+        lses.append(lse.cpu().numpy())
+        bufs.append(to_np(kv))
+    for b in bufs:
+        assert np.array_equal(b, kv_ref), "an SP rank's buffer differs"
+    check_out(np.concatenate(outs, axis=1), ref_o, dtype, "sharded queries out")
+    check_lse(np.concatenate(lses, axis=2), ref_l, dtype, "sharded queries lse")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_patch_ranges_update_only_and_no_fresh_rows(orc, torch, dtype):
+    """q_len = 0 only stores the fresh rows; no fresh rows is plain attention
+    over the buffer as it stands."""
+    B, N, H, d = 2, 200, 2, 64
+    kv0 = np.ascontiguousarray(np.stack([random_io((B, N, H, d), dtype, 95),
+                                         random_io((B, N, H, d), dtype, 96)]))
+    ranges = [(150, 50), (10, 30)]
+    fk = random_io((B, 80, H, d), dtype, 97)
+    fv = random_io((B, 80, H, d), dtype, 98)
+    kv = to_gpu(kv0, dtype)
+    e = torch.zeros((B, 0, H, d), device="cuda", dtype=tdtype(dtype))
+    xd.xdit_patch_attn_ranges(e, kv, ranges, to_gpu(fk, dtype), to_gpu(fv, dtype), e)
+    torch.cuda.synchronize()
+    exp = kv0.copy()
+    orc.patch_ranges(np.zeros((B, 0, H, d), np.float32), exp, ranges, fk, fv)
+    assert np.array_equal(to_np(kv), exp)
+    q = random_io((B, 70, H, d), dtype, 99)
+    out = _empty_out(torch, B, 70, H, d, dtype)
+    lse = torch.empty((B, H, 70), device="cuda", dtype=torch.float32)
+    xd.xdit_patch_attn_ranges(to_gpu(q, dtype), kv, [], e, e, out, lse)
+    torch.cuda.synchronize()
+    ref_o, ref_l = orc.attention(q, exp[0], exp[1])
+    check_out(to_np(out), ref_o, dtype, "no fresh rows out")
+    check_lse(lse.cpu().numpy(), ref_l, dtype, "no fresh rows lse")
+    assert np.array_equal(to_np(kv), exp)
+
+
+def test_patch_ranges_single_equals_patch_attn(torch):
+    """One range with the patch's own queries is xdit_patch_attn, bit for bit."""
+    B, N, H, d, off, ln = 2, 300, 2, 72, 70, 150
+    q = to_gpu(random_io((B, ln, H, d), "bf16", 41), "bf16")
+    fk = to_gpu(random_io((B, ln, H, d), "bf16", 42), "bf16")
+    fv = to_gpu(random_io((B, ln, H, d), "bf16", 43), "bf16")
+    kv0 = np.ascontiguousarray(np.stack([random_io((B, N, H, d), "bf16", 44),
+                                         random_io((B, N, H, d), "bf16", 45)]))
+    kv1, kv2 = to_gpu(kv0, "bf16"), to_gpu(kv0, "bf16")
+    o1 = _empty_out(torch, B, ln, H, d, "bf16")
+    o2 = _empty_out(torch, B, ln, H, d, "bf16")
+    xd.xdit_patch_attn(q, kv1, off, ln, fk, fv, o1)
+    xd.xdit_patch_attn_ranges(q, kv2, [(off, ln)], fk, fv, o2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(kv1, kv2)
