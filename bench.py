@@ -66,7 +66,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="pixart",
-                    choices=["tiny", "pixart", "sd3", "flux", "cog"])
+                    choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "pixart_hybrid"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
     return ap.parse_args()
@@ -85,13 +85,14 @@ def cpu_baseline(w, t, target_s: float):
     jobs = []  # (description, nq_total, nk, run(rows))
     if w.patches():
         kv = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
-        for p, (off, ln) in enumerate(w.patches()):
-            q = t.q[:, off:off + ln].copy()
-            fk = t.k_fresh[:, off:off + ln].copy()
-            fv = t.v_fresh[:, off:off + ln].copy()
-            jobs.append((f"patch step {p}", ln, w.N,
-                         lambda rows, q=q, off=off, fk=fk, fv=fv: orc.patch(q, kv, off, fk, fv,
-                                                                           rows=rows)))
+        for p, (ranges, qrows) in enumerate(w.patch_calls()):
+            frows = np.concatenate([np.arange(o, o + n) for o, n in ranges])
+            q = t.q[:, qrows].copy()
+            fk = t.k_fresh[:, frows].copy()
+            fv = t.v_fresh[:, frows].copy()
+            jobs.append((f"patch step {p}", len(qrows), w.N,
+                         lambda rows, q=q, ranges=ranges, fk=fk, fv=fv:
+                         orc.patch_ranges(q, kv, ranges, fk, fv, rows=rows)))
     else:
         q0, q1 = w.sp_q
         q = t.q[:, q0:q1].copy()
@@ -328,7 +329,12 @@ def main():
                    " M=8 patch steps",
             "flux": "flux-2048px SP share: B=1 H=24 d=128, Q 4224 rows x 4 chunks of 4224 + merge",
             "cog": "cogvideox video: B=1 H=48 d=64, 17550 video + 226 text tokens, M=16 patch"
-                   " steps + 8-chunk split (Q all rows) + merge"}[w.name]
+                   " steps + 8-chunk split (Q all rows) + merge",
+            "sd3_ic": "sd3-1024px in-context: B=2 H=24 d=64, 4096 image + 333 text tokens,"
+                      " M=8 patch steps, patch 0 carries the text (845 fresh rows and queries)",
+            "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"
+                             " 4096 tokens, M=4 patch steps of 1024 gathered fresh rows,"
+                             " 512 local queries each"}[w.name]
     line = {
         "metric": "attention TFLOP/s (bf16) per patch/chunk step; merge GB/s",
         "value": round(value, 2),

@@ -2,8 +2,10 @@
 
 A step is one pass over every part of the path for one layer:
   * the PipeFusion patch steps p = 0..M-1 in order over the layer's K/V
-    buffer (each call updates patch p's slice and attends over the buffer;
-    Section 4.1.2), and
+    buffer (each call updates patch p's rows, plus the text rows for patch 0
+    with in-context conditioning, and attends over the buffer with the
+    patch's queries, or this GPU's shard of them under hybrid parallelism;
+    Sections 4.1.2 and 4.1.4), and
   * the sequence-parallel share: chunk attention of the local query shard
     against each K/V chunk, then the log-sum-exp merge of the partials
     (Section 4.1.1).
@@ -16,7 +18,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import xdit_chunk_attn, xdit_lse_merge, xdit_patch_attn
+from . import xdit_chunk_attn, xdit_lse_merge, xdit_patch_attn, xdit_patch_attn_ranges
 from .inputs import Tensors, Workload
 
 
@@ -36,12 +38,15 @@ class HotPath:
         # fresh text rows
         self.kv_stale = up(np.stack([t.k_stale, t.v_stale]))
         self.kv_buf = self.kv_stale.clone()
+        # per patch step: fresh ranges and query rows (see Workload.patch_calls)
+        self.calls = w.patch_calls()
         self.patch_q, self.patch_k, self.patch_v, self.patch_out = [], [], [], []
-        for off, ln in w.patches():
-            self.patch_q.append(up(t.q[:, off:off + ln]))
-            self.patch_k.append(up(t.k_fresh[:, off:off + ln]))
-            self.patch_v.append(up(t.v_fresh[:, off:off + ln]))
-            self.patch_out.append(torch.empty((B, ln, H, d), device=device, dtype=dt))
+        for ranges, qrows in self.calls:
+            frows = np.concatenate([np.arange(o, o + n) for o, n in ranges])
+            self.patch_q.append(up(t.q[:, qrows]))
+            self.patch_k.append(up(t.k_fresh[:, frows]))
+            self.patch_v.append(up(t.v_fresh[:, frows]))
+            self.patch_out.append(torch.empty((B, len(qrows), H, d), device=device, dtype=dt))
         self.sp_q = self.sp_out = self.sp_lse = None
         self.chunk_k, self.chunk_v, self.chunk_out, self.chunk_lse = [], [], [], []
         if w.sp_chunks:
@@ -61,9 +66,14 @@ class HotPath:
         self.kv_buf.copy_(self.kv_stale)
 
     def patch_step(self, p: int) -> None:
-        off, ln = self.w.patches()[p]
-        xdit_patch_attn(self.patch_q[p], self.kv_buf, off, ln, self.patch_k[p], self.patch_v[p],
-                        self.patch_out[p])
+        ranges, qrows = self.calls[p]
+        if len(ranges) == 1 and len(qrows) == ranges[0][1]:
+            off, ln = ranges[0]
+            xdit_patch_attn(self.patch_q[p], self.kv_buf, off, ln, self.patch_k[p],
+                            self.patch_v[p], self.patch_out[p])
+        else:
+            xdit_patch_attn_ranges(self.patch_q[p], self.kv_buf, ranges, self.patch_k[p],
+                                   self.patch_v[p], self.patch_out[p])
 
     def chunk_step(self, r: int) -> None:
         xdit_chunk_attn(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
@@ -83,7 +93,7 @@ class HotPath:
 
     # -- accounting ----------------------------------------------------------
     def patch_flops(self, p: int) -> float:
-        return self.w.attn_flops(self.w.patches()[p][1], self.w.N)
+        return self.w.attn_flops(len(self.calls[p][1]), self.w.N)
 
     def chunk_flops(self, r: int) -> float:
         s, e = self.w.sp_chunks[r]
@@ -105,7 +115,7 @@ class HotPath:
         return n * (o + lse) + o + lse
 
     def update_bytes(self, p: int) -> float:
-        """K and V slice: read from the fresh tensors and written to the buffer."""
+        """K and V fresh rows: read from the fresh tensors and written to the buffer."""
         w = self.w
-        ln = w.patches()[p][1]
+        ln = sum(n for _, n in self.calls[p][0])
         return 2 * 2 * w.B * ln * w.H * w.d * w.esize

@@ -34,6 +34,10 @@ class Workload:
     # sequence-parallel leg: query rows and K/V chunk boundaries (row ranges)
     sp_q: tuple = ()      # (start, stop) of the query rows of the local shard
     sp_chunks: tuple = ()  # ((start, stop), ...) K/V row ranges, one per chunk
+    # PipeFusion variants (Sections 4.1.2 and 4.1.4)
+    in_context: bool = False  # the text rows travel with patch 0
+    sp_degree: int = 1        # hybrid SP x PipeFusion: this GPU's queries are the
+                              # first 1/sp_degree of each patch step's query rows
     note: str = ""
 
     @property
@@ -52,6 +56,22 @@ class Workload:
             out.append((off, ln))
             off += ln
         return out
+
+    def patch_calls(self):
+        """Per patch step: (fresh ranges [(off, len), ...], query rows).  The
+        fresh rows are the patch's image rows, plus the text rows for patch 0
+        when in_context; the query rows are those rows, cut to this GPU's
+        first shard of sp_degree when sp_degree > 1."""
+        calls = []
+        for p, (off, ln) in enumerate(self.patches()):
+            ranges = [(off, ln)]
+            if self.in_context and p == 0 and self.n_txt > 0:
+                ranges.append((self.n_img, self.n_txt))
+            rows = np.concatenate([np.arange(o, o + n) for o, n in ranges]).astype(np.int64)
+            if self.sp_degree > 1:
+                rows = rows[:(len(rows) + self.sp_degree - 1) // self.sp_degree]
+            calls.append((ranges, rows))
+        return calls
 
     def attn_flops(self, nq: int, nk: int) -> float:
         """Algorithmic attention FLOPs, 4*B*H*Nq*Nk*d (QK^T and PV)."""
@@ -81,6 +101,13 @@ WORKLOADS = {
                        note="Pixart 1024px: 128x128 latent, 2x2 patchify, CFG pair"),
     "sd3": Workload("sd3", "bf16", 2, 24, 64, 4096, 333, 8, 2,
                     note="SD3 joint attention: 4096 image + 333 text tokens"),
+    "sd3_ic": Workload("sd3_ic", "bf16", 2, 24, 64, 4096, 333, 8, 2, in_context=True,
+                       note="SD3 with in-context conditioning: the 333 text tokens travel"
+                            " with patch 0"),
+    "pixart_hybrid": Workload("pixart_hybrid", "bf16", 2, 16, 72, 4096, 0, 4, 1, sp_degree=2,
+                              note="Pixart 1024px, PipeFusion x 2-way sequence parallelism:"
+                                   " gathered fresh K/V, this GPU's half of each patch's"
+                                   " queries"),
     "flux": Workload("flux", "bf16", 1, 24, 128, 16384, 512, 0, 3,
                      sp_q=(0, 4224), sp_chunks=_even_chunks(16896, 4),
                      note="Flux 2048px sequence-parallel share: 4 shards of 4096 image"

@@ -45,3 +45,11 @@ def test_workload_geometry():
     assert sd3.N == 4429 and [ln for _, ln in sd3.patches()] == [512] * 8
     px = WORKLOADS["pixart"]
     assert px.attn_flops(1024, 4096) == 4 * 2 * 16 * 1024 * 4096 * 72
+    ic = WORKLOADS["sd3_ic"].patch_calls()
+    assert ic[0][0] == [(0, 512), (4096, 333)] and len(ic[0][1]) == 845
+    assert list(ic[0][1][:512]) == list(range(512)) and list(ic[0][1][512:]) == list(range(4096, 4429))
+    assert all(r == [(512 * p, 512)] and len(q) == 512 for p, (r, q) in enumerate(ic) if p > 0)
+    hy = WORKLOADS["pixart_hybrid"].patch_calls()
+    assert all(r == [(1024 * p, 1024)] and list(q) == list(range(1024 * p, 1024 * p + 512))
+               for p, (r, q) in enumerate(hy))
+    assert [len(q) for _, q in WORKLOADS["cog"].patch_calls()] == lens

@@ -24,7 +24,7 @@ def _rows(w, n: int, target: int, extra=()):
     return sample_rows(n, step, edges)
 
 
-@pytest.mark.parametrize("name", ["tiny", "pixart", "sd3", "cog"])
+@pytest.mark.parametrize("name", ["tiny", "pixart", "sd3", "cog", "sd3_ic", "pixart_hybrid"])
 def test_patch_steps_full_size(name):
     torch = torch_mod()
     orc = oracle.get()
@@ -33,17 +33,19 @@ def test_patch_steps_full_size(name):
     hp = HotPath(w, t)
     kv_ref = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
     target = 24 if w.N > 10000 else 48
-    print(f"[{name}] {len(w.patches())} patch steps over {w.N} rows", flush=True)
-    for p, (off, ln) in enumerate(w.patches()):
+    calls = w.patch_calls()
+    print(f"[{name}] {len(calls)} patch steps over {w.N} rows", flush=True)
+    for p, (ranges, qrows) in enumerate(calls):
         hp.patch_step(p)
         torch.cuda.synchronize()
-        rows = _rows(w, ln, target)
-        ref_o, _ = orc.patch(t.q[:, off:off + ln].copy(), kv_ref, off,
-                             t.k_fresh[:, off:off + ln].copy(), t.v_fresh[:, off:off + ln].copy(),
-                             rows=rows)
+        rows = _rows(w, len(qrows), target, extra=[ranges[0][1] - 1, ranges[0][1]])
+        frows = np.concatenate([np.arange(o, o + n) for o, n in ranges])
+        ref_o, _ = orc.patch_ranges(t.q[:, qrows].copy(), kv_ref, ranges,
+                                    t.k_fresh[:, frows].copy(), t.v_fresh[:, frows].copy(),
+                                    rows=rows)
         got = to_np(hp.patch_out[p])[:, rows]
         check_out(got, ref_o, w.dtype, f"{name} patch {p}")
-        if p in (0, len(w.patches()) - 1) or w.name == "tiny":
+        if p in (0, len(calls) - 1) or w.name == "tiny":
             assert np.array_equal(to_np(hp.kv_buf), kv_ref), f"{name}: buffer after patch {p}"
     # after the last patch every image row is fresh; text rows never changed
     assert np.array_equal(kv_ref[0], t.k_fresh) and np.array_equal(kv_ref[1], t.v_fresh)
