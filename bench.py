@@ -66,7 +66,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="pixart",
-                    choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "pixart_hybrid"])
+                    choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "pixart_hybrid",
+                             "flux_ring"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
     return ap.parse_args()
@@ -173,7 +174,8 @@ def main():
     if hp.sp_q is not None:
         for r in range(len(hp.chunk_k)):
             calls.append(("chunk_attn", lambda r=r: hp.chunk_step(r), hp.chunk_flops(r), 0.0))
-        calls.append(("lse_merge", hp.merge, 0.0, hp.merge_bytes()))
+        if not w.sp_ring:
+            calls.append(("lse_merge", hp.merge, 0.0, hp.merge_bytes()))
 
     for _ in range(args.warmup):
         hp.step()
@@ -276,7 +278,7 @@ def main():
 
     # the merge is one launch per step, so its in-step events include their
     # own overhead; back-to-back launches through the C ABI give its duration
-    if hp.sp_q is not None:
+    if hp.sp_q is not None and not w.sp_ring:
         import ctypes
 
         L = _lib.lib()
@@ -332,6 +334,8 @@ def main():
                    " steps + 8-chunk split (Q all rows) + merge",
             "sd3_ic": "sd3-1024px in-context: B=2 H=24 d=64, 4096 image + 333 text tokens,"
                       " M=8 patch steps, patch 0 carries the text (845 fresh rows and queries)",
+            "flux_ring": "flux-2048px SP share, ring form: B=1 H=24 d=128, Q 4224 rows, 4 chunks"
+                         " of 4224 each merged into the running output as it arrives",
             "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"
                              " 4096 tokens, M=4 patch steps of 1024 gathered fresh rows,"
                              " 512 local queries each"}[w.name]

@@ -140,6 +140,24 @@ int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, floa
                     int64_t head_dim, int32_t dtype);
 
 /*
+ * Ring step with the merge fused in (Section 4.1.1: SP-Ring accumulates the
+ * partial attention of each K/V sub-block it receives).  Attention of q over
+ * one K/V chunk is merged into the running output and log-sum-exp of the
+ * chunks before it:
+ *   L = ln(e^{lse} + e^{lse_c}),  out = e^{lse - L} * out + e^{lse_c - L} * o_c
+ * with (o_c, lse_c) this chunk's attention; out and lse are read, then
+ * overwritten with the merged state.  A running lse of -inf marks an empty
+ * state: its out is ignored (it may hold anything, NaN included), so a ring
+ * starts from lse = -inf or from xdit_chunk_attn's result.  After every chunk
+ * of the sequence, out and lse equal attention over the whole sequence.
+ * Arguments and requirements as for xdit_chunk_attn, except that lse is
+ * required.  The running out is stored in the I/O dtype after every step.
+ */
+int xdit_chunk_attn_accum(const void* q, const void* k, const void* v, void* out, float* lse,
+                          int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                          int64_t head_dim, int32_t dtype);
+
+/*
  * Log-sum-exp merge of n chunk partials into attention over the union of the
  * chunks (Section 4.1.1: the sharded computation gives the serial result):
  *   M = max_r lse_r,  L = M + ln sum_r exp(lse_r - M),

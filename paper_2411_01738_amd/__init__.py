@@ -16,7 +16,8 @@ import ctypes
 from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XditError, check,
                    lib)
 
-__all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn", "xdit_lse_merge",
+__all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
+           "xdit_chunk_attn_accum", "xdit_lse_merge",
            "xdit_kv_update", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
            "version"]
 
@@ -117,9 +118,7 @@ def xdit_patch_attn_ranges(q, kv_buf, ranges, fresh_k, fresh_v, out, lse=None) -
                                        _dtype_code(kv_buf)))
 
 
-def xdit_chunk_attn(q, k, v, out, lse=None) -> None:
-    """Chunk attention: out = attention(q, k, v) and, if given,
-    lse [B,H,Nq] = log-sum-exp of the scaled scores (natural log)."""
+def _chunk_args(q, k, v, out, lse):
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out")):
         _dense(t, n, 4)
     _dense(lse, "lse", 3)
@@ -136,9 +135,25 @@ def xdit_chunk_attn(q, k, v, out, lse=None) -> None:
         torch = _torch()
         if lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, Nq):
             raise XditError(-3, f"lse must be float32 [B,H,Nq] = {(B, H, Nq)}")
+    return (_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Nq, Nk, H, d, _dtype_code(q))
+
+
+def xdit_chunk_attn(q, k, v, out, lse=None) -> None:
+    """Chunk attention: out = attention(q, k, v) and, if given,
+    lse [B,H,Nq] = log-sum-exp of the scaled scores (natural log)."""
+    args = _chunk_args(q, k, v, out, lse)
     _use_current_stream()
-    check(lib().xdit_chunk_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Nq, Nk, H, d,
-                                _dtype_code(q)))
+    check(lib().xdit_chunk_attn(*args))
+
+
+def xdit_chunk_attn_accum(q, k, v, out, lse) -> None:
+    """Ring step: merge attention(q, k, v) into the running (out, lse) in
+    place.  lse = -inf marks an empty running state (out then ignored)."""
+    if lse is None:
+        raise XditError(-1, "the running lse is required")
+    args = _chunk_args(q, k, v, out, lse)
+    _use_current_stream()
+    check(lib().xdit_chunk_attn_accum(*args))
 
 
 def xdit_lse_merge(outs, lses, n: int, out, lse_out=None) -> None:

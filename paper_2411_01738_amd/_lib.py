@@ -33,6 +33,8 @@ SIGNATURES = {
     "xdit_patch_attn_ranges": (ctypes.c_int, [_vp, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                               _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
+    "xdit_chunk_attn_accum": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
+                                             _i32]),
     "xdit_lse_merge": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_kv_update": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_set_stream": (ctypes.c_int, [_vp]),

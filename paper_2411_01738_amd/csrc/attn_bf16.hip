@@ -125,6 +125,7 @@ struct Args {
     int B, H, Nq, Nk, q_tiles;
     int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
     float c2;  // softmax scale * log2(e)
+    int accum;  // merge into the running (out, lse) instead of overwriting them
 };
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
@@ -659,6 +660,31 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         l_tot = halves_sum(l_run);
     }
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    constexpr float kLn2 = 0.69314718055994531f;
+    const float lse_new = l_tot > 0.f ? (m_ref * a.c2 + __log2f(l_tot)) * kLn2 : -INFINITY;
+    const int64_t lidx = ((int64_t)b * a.H + hh) * a.Nq + qrow;
+    // Merge into a running (out, lse) (the ring's accumulation over chunks,
+    // Section 4.1.1): weights e^{lse_prev - L} and e^{lse_new - L} with
+    // L = ln(e^{lse_prev} + e^{lse_new}); a running lse of -inf marks an empty
+    // state whose output is ignored.
+    float w_prev = 0.f, w_new = inv, lse_out = lse_new;
+    if (a.accum) {
+        const float lse_prev = qvalid ? a.lse[lidx] : -INFINITY;
+        if (lse_prev != -INFINITY) {
+            if (lse_new == -INFINITY) {
+                w_prev = 1.f;
+                w_new = 0.f;
+                lse_out = lse_prev;
+            } else {
+                const float M = fmaxf(lse_prev, lse_new);
+                const float e1 = __expf(lse_prev - M), e2 = __expf(lse_new - M);
+                const float rs = 1.f / (e1 + e2);
+                w_prev = e1 * rs;
+                w_new = e2 * rs * inv;
+                lse_out = M + __logf(e1 + e2);
+            }
+        }
+    }
 #pragma unroll
     for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
@@ -667,16 +693,24 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             const int dim = 32 * db + 8 * g + 4 * hf;
             if (dim < D) {
                 const f32x16& o16 = oacc[db];
-                const u32x2 w = {pack_bf16x2(o16[4 * g] * inv, o16[4 * g + 1] * inv),
-                                 pack_bf16x2(o16[4 * g + 2] * inv, o16[4 * g + 3] * inv)};
                 const uint32_t o = qvalid ? (uint32_t)qrow * rowb + headb + 2 * dim : kOOB;
+                float y[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) y[e] = o16[4 * g + e] * w_new;
+                if (w_prev != 0.f) {
+                    const u32x2 pv = __builtin_amdgcn_raw_buffer_load_b64(ro, o, 0, 0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t h = pv[e >> 1];
+                        const float x = __uint_as_float((e & 1) ? (h & 0xffff0000u) : (h << 16));
+                        y[e] = __builtin_fmaf(w_prev, x, y[e]);
+                    }
+                }
+                const u32x2 w = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
                 __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
             }
         }
-    if (a.lse && hf == 0 && qvalid) {
-        const float lse = l_tot > 0.f ? (m_ref * a.c2 + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-        a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = lse;
-    }
+    if (a.lse && hf == 0 && qvalid) a.lse[lidx] = lse_out;
 }
 
 template <int D, int QB, int KS, int KW, bool PATCH>
@@ -702,6 +736,7 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.len1 = p.len1;
     a.q_tiles = (p.Nq + C::BM - 1) / C::BM;
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
+    a.accum = p.accum;
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),

@@ -31,6 +31,7 @@ struct Args {
     int B, H, Nq, Nk, q_tiles;
     int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
     float scale;
+    int accum;  // merge into the running (out, lse) instead of overwriting them
 };
 
 __device__ __forceinline__ int xcd_remap(int pid, int total) {
@@ -133,11 +134,38 @@ __global__ __launch_bounds__(kFBM) void attn_f32_kernel(Args a) {
 
     if (qvalid) {
         const float inv = l > 0.f ? 1.f / l : 0.f;
+        const float lse_new = l > 0.f ? m + logf(l) : -INFINITY;
+        const int64_t lidx = ((int64_t)b * a.H + hh) * a.Nq + qrow;
+        // merge into a running (out, lse): see the bf16 kernel
+        float w_prev = 0.f, w_new = inv, lse_out = lse_new;
+        if (a.accum) {
+            const float lse_prev = a.lse[lidx];
+            if (lse_prev != -INFINITY) {
+                if (lse_new == -INFINITY) {
+                    w_prev = 1.f;
+                    w_new = 0.f;
+                    lse_out = lse_prev;
+                } else {
+                    const float M = fmaxf(lse_prev, lse_new);
+                    const float e1 = expf(lse_prev - M), e2 = expf(lse_new - M);
+                    w_prev = e1 / (e1 + e2);
+                    w_new = e2 / (e1 + e2) * inv;
+                    lse_out = M + logf(e1 + e2);
+                }
+            }
+        }
         float* op = a.out + ((int64_t)b * a.Nq + qrow) * rs + (int64_t)hh * D;
 #pragma unroll
-        for (int c = 0; c < D; c += 4)
-            *(f32x4*)(op + c) = f32x4{o[c] * inv, o[c + 1] * inv, o[c + 2] * inv, o[c + 3] * inv};
-        if (a.lse) a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = l > 0.f ? m + logf(l) : -INFINITY;
+        for (int c = 0; c < D; c += 4) {
+            f32x4 y = {o[c] * w_new, o[c + 1] * w_new, o[c + 2] * w_new, o[c + 3] * w_new};
+            if (w_prev != 0.f) {
+                const f32x4 x = *(const f32x4*)(op + c);
+                y = f32x4{__builtin_fmaf(w_prev, x[0], y[0]), __builtin_fmaf(w_prev, x[1], y[1]),
+                          __builtin_fmaf(w_prev, x[2], y[2]), __builtin_fmaf(w_prev, x[3], y[3])};
+            }
+            *(f32x4*)(op + c) = y;
+        }
+        if (a.lse) a.lse[lidx] = lse_out;
     }
 }
 
@@ -163,6 +191,7 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.len1 = p.len1;
     a.q_tiles = (p.Nq + kFBM - 1) / kFBM;
     a.scale = (float)(1.0 / sqrt((double)D));
+    a.accum = p.accum;
     const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((attn_f32_kernel<D, PATCH>), dim3((unsigned)blocks), dim3(kFBM), 0, s, a);

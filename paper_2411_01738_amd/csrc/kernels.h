@@ -24,6 +24,7 @@ struct AttnParams {
     int B, H, Nq, Nk, D;
     int off0, len0;       // first fresh range
     int off1, len1;       // second fresh range (len1 == 0: none); disjoint from the first
+    int accum;            // merge into the running (out, lse) instead of overwriting them
 };
 
 struct MergeParams {

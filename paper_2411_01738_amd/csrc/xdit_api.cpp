@@ -110,13 +110,12 @@ const char* xdit_last_error(void) { return g_error; }
 
 const char* xdit_version(void) { return "xdit-mi355x 0.1 (gfx950)"; }
 
-int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, float* lse,
-                    int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
-                    int32_t dtype) {
-    clear_error();
+static int chunk_impl(const char* fn, const void* q, const void* k, const void* v, void* out,
+                      float* lse, int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                      int64_t head_dim, int32_t dtype, int accum) {
     XDIT_TRY(check_dtype_dim(dtype, head_dim));
-    XDIT_TRY(check_dims("xdit_chunk_attn", batch, q_len, kv_len, heads));
-    XDIT_TRY(check_batch_bytes("xdit_chunk_attn", q_len > kv_len ? q_len : kv_len, heads, head_dim,
+    XDIT_TRY(check_dims(fn, batch, q_len, kv_len, heads));
+    XDIT_TRY(check_batch_bytes(fn, q_len > kv_len ? q_len : kv_len, heads, head_dim,
                                esize_of(dtype)));
     const int64_t es = esize_of(dtype);
     const int64_t row = heads * head_dim * es;
@@ -124,6 +123,8 @@ int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, floa
         sv{v, batch * kv_len * row, "v"}, so{out, batch * q_len * row, "out"},
         sl{lse, lse ? batch * heads * q_len * 4 : 0, "lse"};
     for (const Span* s : {&sq, &sk, &sv, &so}) XDIT_TRY(check_ptr(*s));
+    if (accum && lse == nullptr && batch * heads * q_len > 0)
+        return fail(XDIT_ERR_NULL, "%s: the running lse is required", fn);
     if (lse && ((uintptr_t)lse & 3u)) return fail(XDIT_ERR_LAYOUT, "lse is not 4-byte aligned");
     for (const Span* s : {&sq, &sk, &sv}) {
         XDIT_TRY(check_no_overlap(so, *s));
@@ -143,9 +144,26 @@ int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, floa
     p.Nq = (int)q_len;
     p.Nk = (int)kv_len;
     p.D = (int)head_dim;
+    p.accum = accum;
     const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
                                             : xdit::launch_attn_f32(p, g_stream);
-    return hip_status(e, "xdit_chunk_attn launch");
+    return hip_status(e, fn);
+}
+
+int xdit_chunk_attn(const void* q, const void* k, const void* v, void* out, float* lse,
+                    int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
+                    int32_t dtype) {
+    clear_error();
+    return chunk_impl("xdit_chunk_attn", q, k, v, out, lse, batch, q_len, kv_len, heads, head_dim,
+                      dtype, 0);
+}
+
+int xdit_chunk_attn_accum(const void* q, const void* k, const void* v, void* out, float* lse,
+                          int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                          int64_t head_dim, int32_t dtype) {
+    clear_error();
+    return chunk_impl("xdit_chunk_attn_accum", q, k, v, out, lse, batch, q_len, kv_len, heads,
+                      head_dim, dtype, 1);
 }
 
 static int check_patch_args(const char* fn, const void* q, void* kv_buf, int64_t patch_off,

@@ -18,7 +18,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import xdit_chunk_attn, xdit_lse_merge, xdit_patch_attn, xdit_patch_attn_ranges
+from . import (xdit_chunk_attn, xdit_chunk_attn_accum, xdit_lse_merge, xdit_patch_attn,
+               xdit_patch_attn_ranges)
 from .inputs import Tensors, Workload
 
 
@@ -56,8 +57,10 @@ class HotPath:
             for s, e in w.sp_chunks:
                 self.chunk_k.append(up(t.k_fresh[:, s:e]))
                 self.chunk_v.append(up(t.v_fresh[:, s:e]))
-                self.chunk_out.append(torch.empty((B, nq, H, d), device=device, dtype=dt))
-                self.chunk_lse.append(torch.empty((B, H, nq), device=device, dtype=torch.float32))
+                if not w.sp_ring:
+                    self.chunk_out.append(torch.empty((B, nq, H, d), device=device, dtype=dt))
+                    self.chunk_lse.append(torch.empty((B, H, nq), device=device,
+                                                      dtype=torch.float32))
             self.sp_out = torch.empty((B, nq, H, d), device=device, dtype=dt)
             self.sp_lse = torch.empty((B, H, nq), device=device, dtype=torch.float32)
 
@@ -76,11 +79,19 @@ class HotPath:
                                    self.patch_v[p], self.patch_out[p])
 
     def chunk_step(self, r: int) -> None:
-        xdit_chunk_attn(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
-                        self.chunk_lse[r])
+        if self.w.sp_ring:
+            # ring form: the first chunk starts the running (out, lse), the
+            # others are merged into it
+            f = xdit_chunk_attn if r == 0 else xdit_chunk_attn_accum
+            f(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.sp_out, self.sp_lse)
+        else:
+            xdit_chunk_attn(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
+                            self.chunk_lse[r])
 
     def merge(self) -> None:
         n = len(self.chunk_out)
+        if n == 0:
+            return
         xdit_lse_merge(self.chunk_out, self.chunk_lse, n, self.sp_out, self.sp_lse)
 
     def step(self) -> None:
@@ -89,7 +100,8 @@ class HotPath:
         if self.sp_q is not None:
             for r in range(len(self.chunk_k)):
                 self.chunk_step(r)
-            self.merge()
+            if not self.w.sp_ring:
+                self.merge()
 
     # -- accounting ----------------------------------------------------------
     def patch_flops(self, p: int) -> float:

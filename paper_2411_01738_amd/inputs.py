@@ -38,6 +38,8 @@ class Workload:
     in_context: bool = False  # the text rows travel with patch 0
     sp_degree: int = 1        # hybrid SP x PipeFusion: this GPU's queries are the
                               # first 1/sp_degree of each patch step's query rows
+    sp_ring: bool = False     # SP chunks merged into a running (out, lse) one by one
+                              # instead of stored as partials and merged at the end
     note: str = ""
 
     @property
@@ -112,6 +114,10 @@ WORKLOADS = {
                      sp_q=(0, 4224), sp_chunks=_even_chunks(16896, 4),
                      note="Flux 2048px sequence-parallel share: 4 shards of 4096 image"
                           " + 128 text tokens; Q is shard 0"),
+    "flux_ring": Workload("flux_ring", "bf16", 1, 24, 128, 16384, 512, 0, 3,
+                          sp_q=(0, 4224), sp_chunks=_even_chunks(16896, 4), sp_ring=True,
+                          note="Flux 2048px sequence-parallel share, ring form: each chunk"
+                               " is merged into the running output as it arrives"),
     "cog": Workload("cog", "bf16", 1, 48, 64, 17550, 226, 16, 4,
                     sp_q=(0, 17776), sp_chunks=_even_chunks(17776, 8),
                     note="CogVideoX video: 13x30x45 latent grid + 226 text tokens"),

@@ -27,9 +27,9 @@ def header_functions():
 
 def test_header_declares_the_entry_points():
     names = header_functions()
-    for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn", "xdit_lse_merge",
-               "xdit_kv_update", "xdit_set_stream", "xdit_get_stream", "xdit_last_error",
-               "xdit_version"]:
+    for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
+               "xdit_chunk_attn_accum", "xdit_lse_merge", "xdit_kv_update", "xdit_set_stream",
+               "xdit_get_stream", "xdit_last_error", "xdit_version"]:
         assert fn in names
 
 
@@ -80,6 +80,9 @@ def P(i):
     (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(0) + 64, P(4), 1, 16, 16, 2, 64, 0), -6),
     (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(2), 1, 16, 16, 2, 64, 0), -6),
     (lambda L: L.xdit_chunk_attn(P(0), P(1), P(2), P(3), P(3) + 16, 1, 16, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_chunk_attn_accum(P(0), P(1), P(2), P(3), None, 1, 16, 16, 2, 64, 0), -1),
+    (lambda L: L.xdit_chunk_attn_accum(P(0), P(1), P(2), P(3), P(3) + 16, 1, 16, 16, 2, 64, 0), -6),
+    (lambda L: L.xdit_chunk_attn_accum(P(0), P(1), P(2), P(3), P(4), 1, 16, 16, 2, 72, 5), -2),
     (lambda L: L.xdit_patch_attn(P(0), P(1), 10, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),
     (lambda L: L.xdit_patch_attn(P(0), P(1), -1, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),
     (lambda L: L.xdit_patch_attn(P(0), P(1), 0, -8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -4),

@@ -427,3 +427,48 @@ def test_patch_ranges_single_equals_patch_attn(torch):
     xd.xdit_patch_attn_ranges(q, kv2, [(off, ln)], fk, fv, o2)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2) and torch.equal(kv1, kv2)
+
+
+# ---------------------------------------------------------------------------
+# Ring step with the merge fused in
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 72), ("bf16", 128), ("f32", 64),
+                                     ("f32", 128)])
+def test_ring_accum_equals_full(orc, torch, tile_shape, dtype, d):
+    """Chunks merged one by one into a running (out, lse) that starts empty
+    (lse = -inf, out NaN) give attention over the whole sequence; an empty
+    chunk leaves the running state bit for bit."""
+    B, Nq, H, Nk = 2, 130, 2, 357
+    chunks = [(0, 100), (100, 200), (200, 200), (200, 357)]
+    q = random_io((B, Nq, H, d), dtype, 300 + d)
+    k = random_io((B, Nk, H, d), dtype, 301 + d)
+    v = random_io((B, Nk, H, d), dtype, 302 + d)
+    qg = to_gpu(q, dtype)
+    out = _empty_out(torch, B, Nq, H, d, dtype)
+    lse = torch.full((B, H, Nq), float("-inf"), device="cuda", dtype=torch.float32)
+    for s, e in chunks:
+        before = (out.clone(), lse.clone())
+        xd.xdit_chunk_attn_accum(qg, to_gpu(k[:, s:e], dtype), to_gpu(v[:, s:e], dtype), out, lse)
+        torch.cuda.synchronize()
+        if s == e:
+            assert torch.equal(out, before[0]) and torch.equal(lse, before[1]), "empty chunk changed the state"
+    ref_o, ref_l = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, dtype, "ring accumulation out")
+    check_lse(lse.cpu().numpy(), ref_l, dtype, "ring accumulation lse")
+
+
+def test_ring_accum_continues_chunk_attn(orc, torch):
+    """A ring may start from xdit_chunk_attn's output for its first chunk."""
+    B, Nq, H, d = 1, 200, 3, 72
+    q = random_io((B, Nq, H, d), "bf16", 310)
+    k = random_io((B, 600, H, d), "bf16", 311)
+    v = random_io((B, 600, H, d), "bf16", 312)
+    qg = to_gpu(q, "bf16")
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = torch.empty((B, H, Nq), device="cuda", dtype=torch.float32)
+    xd.xdit_chunk_attn(qg, to_gpu(k[:, :256], "bf16"), to_gpu(v[:, :256], "bf16"), out, lse)
+    xd.xdit_chunk_attn_accum(qg, to_gpu(k[:, 256:], "bf16"), to_gpu(v[:, 256:], "bf16"), out, lse)
+    torch.cuda.synchronize()
+    ref_o, ref_l = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, "bf16", "chunk then accum out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", "chunk then accum lse")

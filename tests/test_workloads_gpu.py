@@ -51,7 +51,7 @@ def test_patch_steps_full_size(name):
     assert np.array_equal(kv_ref[0], t.k_fresh) and np.array_equal(kv_ref[1], t.v_fresh)
 
 
-@pytest.mark.parametrize("name", ["tiny", "pixart", "flux", "cog"])
+@pytest.mark.parametrize("name", ["tiny", "pixart", "flux", "cog", "flux_ring"])
 def test_sp_chunks_and_merge_full_size(name):
     torch = torch_mod()
     orc = oracle.get()
@@ -68,7 +68,7 @@ def test_sp_chunks_and_merge_full_size(name):
     rows = _rows(w, nq, 40)
     q = t.q[:, q0:q1].copy()
     for r, (s, e) in enumerate(w.sp_chunks):
-        if w.name != "tiny" and r not in (0, len(w.sp_chunks) - 1):
+        if w.sp_ring or (w.name != "tiny" and r not in (0, len(w.sp_chunks) - 1)):
             continue
         ro, rl = orc.attention(q, t.k_fresh[:, s:e].copy(), t.v_fresh[:, s:e].copy(), rows=rows)
         check_out(to_np(hp.chunk_out[r])[:, rows], ro, w.dtype, f"{name} chunk {r}")
