@@ -68,6 +68,8 @@ def parse():
     ap.add_argument("--workload", default="pixart",
                     choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "pixart_hybrid",
                              "flux_ring"])
+    ap.add_argument("--no-split", action="store_true",
+                    help="never split a query tile's keys over several workgroups")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
     return ap.parse_args()
@@ -164,7 +166,7 @@ def main():
     torch.cuda.set_device(0)
     w = WORKLOADS[args.workload]
     t = generate(w)
-    hp = HotPath(w, t)
+    hp = HotPath(w, t, split=not args.no_split)
     stream = torch.cuda.current_stream()
 
     # each entry: (kind, callable, flops, bytes)

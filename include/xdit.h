@@ -48,6 +48,9 @@ enum { XDIT_BF16 = 0, XDIT_F32 = 1 };
 /* Upper bound on the fresh row ranges of one xdit_patch_attn_ranges call. */
 #define XDIT_MAX_RANGES 2
 
+/* Upper bound on the key splits of one *_split call. */
+#define XDIT_MAX_SPLITS 16
+
 typedef enum {
     XDIT_OK = 0,
     XDIT_ERR_NULL = -1,        /* a required pointer is NULL                  */
@@ -175,6 +178,39 @@ int xdit_chunk_attn_accum(const void* q, const void* k, const void* v, void* out
 int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n, void* out,
                    float* lse_out, int64_t batch, int64_t q_len, int64_t heads,
                    int64_t head_dim, int32_t dtype);
+
+/*
+ * Key-split forms of xdit_chunk_attn and xdit_patch_attn_ranges, for query
+ * counts that leave most of the 256 CUs idle (few query tiles per head).
+ * Each query tile's K/V sweep is cut into `splits` consecutive parts that run
+ * as separate workgroups; every part writes its partial output and
+ * log-sum-exp into the workspace, and the log-sum-exp merge of Section 4.1.1
+ * (the same arithmetic as xdit_lse_merge) combines them into out and lse.
+ * The results equal the unsplit call's up to the bf16 rounding of the
+ * partials.
+ *
+ *   splits     1 .. XDIT_MAX_SPLITS, or <= 0 to let the library choose
+ *              (fewest rounds of workgroups over the CUs per unit of work,
+ *              at least four 128-key tiles per part); 1 = the unsplit call
+ *   workspace  device memory of at least xdit_split_workspace_bytes(...)
+ *              bytes for the same sizes and splits, 256-byte aligned, not
+ *              overlapping any argument; unused (may be NULL) when no split
+ *              happens.  Its contents on entry do not matter.
+ * float32 calls run unsplit.  Other arguments as for the unsplit calls.
+ * The split sweep and the merge are two launches on the calling thread's
+ * stream.
+ */
+int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                                   int64_t head_dim, int32_t dtype, int32_t splits);
+int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out, float* lse,
+                          int32_t splits, void* workspace, int64_t workspace_bytes, int64_t batch,
+                          int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
+                          int32_t dtype);
+int xdit_patch_attn_split(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
+                          const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
+                          const void* fresh_v, void* out, float* lse, int32_t splits,
+                          void* workspace, int64_t workspace_bytes, int64_t batch, int64_t seq_len,
+                          int64_t heads, int64_t head_dim, int32_t dtype);
 
 /*
  * The update half of the patch step on its own (Section 4.1.2): copy the

@@ -13,11 +13,12 @@ from __future__ import annotations
 
 import ctypes
 
-from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XditError, check,
-                   lib)
+from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XDIT_MAX_SPLITS,
+                   XditError, check, lib)
 
 __all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
-           "xdit_chunk_attn_accum", "xdit_lse_merge",
+           "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
+           "split_workspace_bytes", "xdit_lse_merge",
            "xdit_kv_update", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
            "version"]
 
@@ -144,6 +145,52 @@ def xdit_chunk_attn(q, k, v, out, lse=None) -> None:
     args = _chunk_args(q, k, v, out, lse)
     _use_current_stream()
     check(lib().xdit_chunk_attn(*args))
+
+
+def split_workspace_bytes(q, kv_len: int, splits: int = 0) -> int:
+    """Bytes of workspace the *_split calls need for queries shaped like q
+    [B,Nq,H,d] over kv_len keys (0 when no split happens)."""
+    B, Nq, H, d = q.shape
+    n = lib().xdit_split_workspace_bytes(B, Nq, int(kv_len), H, d, _dtype_code(q), int(splits))
+    if n < 0:
+        raise XditError(-3, "xdit_split_workspace_bytes rejected the sizes")
+    return int(n)
+
+
+def _workspace(ws):
+    if ws is None:
+        return None, 0
+    if not ws.is_cuda or not ws.is_contiguous():
+        raise XditError(-5, "workspace must be a dense GPU tensor")
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def xdit_chunk_attn_split(q, k, v, out, lse=None, splits: int = 0, workspace=None) -> None:
+    """xdit_chunk_attn with each query tile's keys split `splits` ways (0: the
+    library chooses); workspace: a GPU tensor of split_workspace_bytes bytes."""
+    args = _chunk_args(q, k, v, out, lse)
+    wp, wb = _workspace(workspace)
+    _use_current_stream()
+    check(lib().xdit_chunk_attn_split(*args[:5], int(splits), wp, wb, *args[5:]))
+
+
+def xdit_patch_attn_split(q, kv_buf, ranges, fresh_k, fresh_v, out, lse=None, splits: int = 0,
+                          workspace=None) -> None:
+    """xdit_patch_attn_ranges with the keys split `splits` ways (0: the
+    library chooses); workspace as for xdit_chunk_attn_split."""
+    _dense(kv_buf, "kv_buf", 5)
+    for t, n in ((q, "q"), (fresh_k, "fresh_k"), (fresh_v, "fresh_v"), (out, "out")):
+        _dense(t, n, 4)
+    _dense(lse, "lse", 3)
+    _, B, N, H, d = kv_buf.shape
+    nr = len(ranges)
+    offs = (ctypes.c_int64 * max(nr, 1))(*[int(r[0]) for r in ranges])
+    lens = (ctypes.c_int64 * max(nr, 1))(*[int(r[1]) for r in ranges])
+    wp, wb = _workspace(workspace)
+    _use_current_stream()
+    check(lib().xdit_patch_attn_split(_ptr(q), q.shape[1], _ptr(kv_buf), nr, offs, lens,
+                                      _ptr(fresh_k), _ptr(fresh_v), _ptr(out), _ptr(lse),
+                                      int(splits), wp, wb, B, N, H, d, _dtype_code(kv_buf)))
 
 
 def xdit_chunk_attn_accum(q, k, v, out, lse) -> None:

@@ -22,6 +22,7 @@ STATUS = {
 XDIT_BF16, XDIT_F32 = 0, 1
 XDIT_MAX_PARTIALS = 64
 XDIT_MAX_RANGES = 2
+XDIT_MAX_SPLITS = 16
 
 _vp = ctypes.c_void_p
 _i64 = ctypes.c_int64
@@ -33,6 +34,11 @@ SIGNATURES = {
     "xdit_patch_attn_ranges": (ctypes.c_int, [_vp, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                               _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
+    "xdit_split_workspace_bytes": (_i64, [_i64, _i64, _i64, _i64, _i64, _i32, _i32]),
+    "xdit_chunk_attn_split": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _i64, _i64,
+                                             _i64, _i64, _i64, _i32]),
+    "xdit_patch_attn_split": (ctypes.c_int, [_vp, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                             _i32, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn_accum": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
                                              _i32]),
     "xdit_lse_merge": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),

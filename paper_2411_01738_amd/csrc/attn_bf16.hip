@@ -126,6 +126,10 @@ struct Args {
     int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
     float c2;  // softmax scale * log2(e)
     int accum;  // merge into the running (out, lse) instead of overwriting them
+    // key splits: split sp of a query tile sweeps K/V tiles [T*sp/S, T*(sp+1)/S)
+    // and writes its partial (O, LSE) at out + sp*out_split, lse + sp*lse_split
+    int splits;
+    int64_t out_split, lse_split;  // elements
 };
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
@@ -222,7 +226,14 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 
     const int logical = xcd_remap(blockIdx.x, gridDim.x);
     const int qt = logical % a.q_tiles;
-    const int bh = logical / a.q_tiles;
+    const int sp = (logical / a.q_tiles) % a.splits;
+    const int bh = logical / a.q_tiles / a.splits;
+    uint16_t* const out_base = a.out + sp * a.out_split;
+    float* const lse_base = a.lse ? a.lse + sp * a.lse_split : nullptr;
+    // this split's K/V tiles; t counts them from 0, tile tb + t of the sequence
+    const int all_tiles = (a.Nk + BN - 1) / BN;
+    const int tb = (int)((int64_t)all_tiles * sp / a.splits);
+    const int ntiles = (int)((int64_t)all_tiles * (sp + 1) / a.splits) - tb;
     const int hh = bh % a.H, b = bh / a.H;
     const uint32_t rowb = (uint32_t)a.H * D * 2;  // bytes between consecutive rows in memory
     const uint32_t headb = (uint32_t)hh * D * 2;  // byte offset of this head in a row
@@ -256,7 +267,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const int qrow = qt * C::BM + qb * 32 + c;
     const bool qvalid = qrow < a.Nq;
     const Rsrc rq = rsrc(a.q + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
-    const Rsrc ro = rsrc(a.out + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
+    const Rsrc ro = rsrc(out_base + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
     bf16x8 qf[C::KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
@@ -269,8 +280,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     // reads the fresh ranges of the buffer: they are taken from the fresh
     // rows.
     if constexpr (PATCH) {
-        const int r0 = (int)((int64_t)F * qt / a.q_tiles);
-        const int r1 = (int)((int64_t)F * (qt + 1) / a.q_tiles);
+        const int share = qt * a.splits + sp, shares = a.q_tiles * a.splits;
+        const int r0 = (int)((int64_t)F * share / shares);
+        const int r1 = (int)((int64_t)F * (share + 1) / shares);
         const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
         const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), 0, a.Nk);
         const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), 0, a.Nk);
@@ -333,7 +345,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 
     // Issue the loads of K and V tile t into stage s.
     auto load_tile = [&](int t, int s) {
-        const int kind = tile_kind(t), lo = t * BN;
+        const int kind = tile_kind(tb + t), lo = (tb + t) * BN;
         unsigned char* kdst = stage(s);
         unsigned char* vdst = stage(s) + C::TILE_BYTES;
         if (kind != kMixed) {
@@ -431,12 +443,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     };
     // keys past the end of a ragged last tile get -inf
     auto mask = [&](int t, f32x16 (&s)[NKB]) {
-        if ((t + 1) * BN > a.Nk) {
+        if ((tb + t + 1) * BN > a.Nk) {
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int key = t * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
+                    const int key = (tb + t) * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
                     if (key >= a.Nk) s[kb][i] = -INFINITY;
                 }
         }
@@ -532,7 +544,6 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     // max of tile t+1 then runs under the PV products.  Scores of tile t
     // live in sc, those of tile t+1 go to sn.  NEXT: there is a tile t+1;
     // MASK: it may be the ragged last tile.
-    const int ntiles = (a.Nk + BN - 1) / BN;
     auto iteration = [&](int t, f32x16 (&sc)[NKB], f32x16 (&sn)[NKB], auto next_c, auto mask_c) {
         constexpr bool NEXT = decltype(next_c)::value, MASK = decltype(mask_c)::value;
         if constexpr (NEXT) {
@@ -669,7 +680,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     // state whose output is ignored.
     float w_prev = 0.f, w_new = inv, lse_out = lse_new;
     if (a.accum) {
-        const float lse_prev = qvalid ? a.lse[lidx] : -INFINITY;
+        const float lse_prev = qvalid ? lse_base[lidx] : -INFINITY;
         if (lse_prev != -INFINITY) {
             if (lse_new == -INFINITY) {
                 w_prev = 1.f;
@@ -710,7 +721,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
             }
         }
-    if (a.lse && hf == 0 && qvalid) a.lse[lidx] = lse_out;
+    if (lse_base && hf == 0 && qvalid) lse_base[lidx] = lse_out;
 }
 
 template <int D, int QB, int KS, int KW, bool PATCH>
@@ -735,9 +746,12 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.off1 = p.off1;
     a.len1 = p.len1;
     a.q_tiles = (p.Nq + C::BM - 1) / C::BM;
+    a.splits = p.splits > 1 ? p.splits : 1;
+    a.out_split = p.out_split;
+    a.lse_split = p.lse_split;
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
     a.accum = p.accum;
-    const int64_t blocks = (int64_t)a.q_tiles * p.H * p.B;
+    const int64_t blocks = (int64_t)a.q_tiles * a.splits * p.H * p.B;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
                        0, s, a);
@@ -773,7 +787,8 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
         return launch<D, 4, 2, 32, PATCH>(p, s);
     } else {
         const int forced = forced_shape();
-        if (forced == 1) return launch<D, 4, 2, 64, PATCH>(p, s);
+        // split keys fill the GPU by themselves: 128-row query tiles
+        if (forced == 1 || p.splits > 1) return launch<D, 4, 2, 64, PATCH>(p, s);
         if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
         const int64_t bh = (int64_t)p.B * p.H;
         const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;

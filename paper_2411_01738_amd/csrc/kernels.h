@@ -25,6 +25,10 @@ struct AttnParams {
     int off0, len0;       // first fresh range
     int off1, len1;       // second fresh range (len1 == 0: none); disjoint from the first
     int accum;            // merge into the running (out, lse) instead of overwriting them
+    // key splits (bf16 only): split s writes its partial at out + s*out_split
+    // and lse + s*lse_split (elements); splits <= 1: no split
+    int splits;
+    int64_t out_split, lse_split;
 };
 
 struct MergeParams {

@@ -110,9 +110,102 @@ const char* xdit_last_error(void) { return g_error; }
 
 const char* xdit_version(void) { return "xdit-mi355x 0.1 (gfx950)"; }
 
+struct SplitArgs {
+    int32_t splits = 1;        // requested (<= 0: the library picks)
+    void* workspace = nullptr;
+    int64_t workspace_bytes = 0;
+};
+
+static constexpr int kCUs = 256;
+static constexpr int kSplitRows = 128;  // query rows per workgroup when keys are split
+
+static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
+
+static int64_t split_ws_bytes(int64_t batch, int64_t q_len, int64_t heads, int64_t head_dim, int es, int s) {
+    return align256((int64_t)s * batch * q_len * heads * head_dim * es) + (int64_t)s * batch * heads * q_len * 4;
+}
+
+// Key splits for a launch of `work` query tiles over `tiles` K/V tiles.
+// Time model in units of one K/V tile of one workgroup: each round of
+// workgroups over the CUs costs a fixed ~4 tiles (prologue, pipeline fill,
+// epilogue) plus its sweep, and a split adds the merge pass (~2 tiles).  A
+// split is taken only when the model saves at least 10 %: with measured
+// per-workgroup overheads, splitting pays only when whole rounds are
+// saved (a tile count well below the CU count).
+static int pick_splits(int64_t work, int64_t tiles) {
+    auto cost = [&](int s) {
+        const double rounds = (double)((work * s + kCUs - 1) / kCUs);
+        return rounds * (4.0 + (double)tiles / s) + (s > 1 ? 2.0 : 0.0);
+    };
+    int best = 1;
+    double best_cost = cost(1);
+    for (int s = 2; s <= XDIT_MAX_SPLITS && tiles >= 4 * s; ++s)
+        if (cost(s) < best_cost) {
+            best_cost = cost(s);
+            best = s;
+        }
+    return best_cost < 0.9 * cost(1) ? best : 1;
+}
+
+// Resolve the split count and check the workspace; returns XDIT_OK and sets
+// *s_out (1 = no split).
+static int resolve_splits(const char* fn, const SplitArgs& sa, int32_t dtype, int64_t batch, int64_t q_len,
+                   int64_t kv_len, int64_t heads, int64_t head_dim, int* s_out) {
+    if (sa.splits > XDIT_MAX_SPLITS)
+        return fail(XDIT_ERR_RANGE, "%s: splits = %d above %d", fn, sa.splits, XDIT_MAX_SPLITS);
+    int s = sa.splits;
+    if (dtype != XDIT_BF16) s = 1;  // the float32 path is not split
+    if (s <= 0) {
+        const int64_t work = (q_len + kSplitRows - 1) / kSplitRows * batch * heads;
+        const int64_t tiles = (kv_len + 127) / 128;
+        s = pick_splits(work, tiles);
+    }
+    if (s > 1) {
+        const int64_t need = split_ws_bytes(batch, q_len, heads, head_dim, esize_of(dtype), s);
+        if (sa.workspace == nullptr || sa.workspace_bytes < need)
+            return fail(XDIT_ERR_RANGE, "%s: workspace of %lld bytes, %d splits need %lld", fn,
+                        (long long)sa.workspace_bytes, s, (long long)need);
+        if ((uintptr_t)sa.workspace & 255u) return fail(XDIT_ERR_LAYOUT, "%s: workspace not 256-byte aligned", fn);
+    }
+    *s_out = s;
+    return XDIT_OK;
+}
+
+// Launch an attention whose keys are split s ways: partials into the
+// workspace, then their log-sum-exp merge into out / lse.
+static hipError_t launch_split(xdit::AttnParams p, int s, void* workspace, int32_t dtype) {
+    const int64_t ob = (int64_t)p.B * p.Nq * p.H * p.D * esize_of(dtype);
+    void* out = p.out;
+    float* lse = p.lse;
+    p.splits = s;
+    p.out = workspace;
+    p.lse = (float*)((char*)workspace + align256((int64_t)s * ob));
+    p.out_split = (int64_t)p.B * p.Nq * p.H * p.D;
+    p.lse_split = (int64_t)p.B * p.H * p.Nq;
+    hipError_t e = xdit::launch_attn_bf16(p, g_stream);
+    if (e != hipSuccess) return e;
+    const void* outs[XDIT_MAX_SPLITS];
+    const float* lses[XDIT_MAX_SPLITS];
+    for (int r = 0; r < s; ++r) {
+        outs[r] = (const char*)workspace + r * ob;
+        lses[r] = p.lse + r * p.lse_split;
+    }
+    xdit::MergeParams m{};
+    m.outs = outs;
+    m.lses = lses;
+    m.n = s;
+    m.out = out;
+    m.lse_out = lse;
+    m.B = p.B;
+    m.Nq = p.Nq;
+    m.H = p.H;
+    m.D = p.D;
+    return xdit::launch_merge_bf16(m, g_stream);
+}
+
 static int chunk_impl(const char* fn, const void* q, const void* k, const void* v, void* out,
                       float* lse, int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
-                      int64_t head_dim, int32_t dtype, int accum) {
+                      int64_t head_dim, int32_t dtype, int accum, const SplitArgs& sa = SplitArgs()) {
     XDIT_TRY(check_dtype_dim(dtype, head_dim));
     XDIT_TRY(check_dims(fn, batch, q_len, kv_len, heads));
     XDIT_TRY(check_batch_bytes(fn, q_len > kv_len ? q_len : kv_len, heads, head_dim,
@@ -131,6 +224,13 @@ static int chunk_impl(const char* fn, const void* q, const void* k, const void* 
         XDIT_TRY(check_no_overlap(sl, *s));
     }
     XDIT_TRY(check_no_overlap(sl, so));
+    int splits = 1;
+    XDIT_TRY(resolve_splits(fn, sa, dtype, batch, q_len, kv_len, heads, head_dim, &splits));
+    if (splits > 1) {
+        const Span sw{sa.workspace, split_ws_bytes(batch, q_len, heads, head_dim, (int)es, splits),
+                      "workspace"};
+        for (const Span* s : {&sq, &sk, &sv, &so, &sl}) XDIT_TRY(check_no_overlap(sw, *s));
+    }
     if (batch == 0 || q_len == 0 || heads == 0) return XDIT_OK;
 
     xdit::AttnParams p{};
@@ -145,6 +245,7 @@ static int chunk_impl(const char* fn, const void* q, const void* k, const void* 
     p.Nk = (int)kv_len;
     p.D = (int)head_dim;
     p.accum = accum;
+    if (splits > 1) return hip_status(launch_split(p, splits, sa.workspace, dtype), fn);
     const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
                                             : xdit::launch_attn_f32(p, g_stream);
     return hip_status(e, fn);
@@ -193,7 +294,7 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
                              int32_t n_ranges, const int64_t* range_off, const int64_t* range_len,
                              const void* fresh_k, const void* fresh_v, void* out, float* lse,
                              int64_t batch, int64_t seq_len, int64_t heads, int64_t head_dim,
-                             int32_t dtype) {
+                             int32_t dtype, const SplitArgs& sa = SplitArgs()) {
     XDIT_TRY(check_dtype_dim(dtype, head_dim));
     if (n_ranges < 0 || n_ranges > XDIT_MAX_RANGES)
         return fail(XDIT_ERR_RANGE, "%s: n_ranges = %d outside [0, %d]", fn, n_ranges, XDIT_MAX_RANGES);
@@ -229,6 +330,12 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
         XDIT_TRY(check_no_overlap(sl, *s));
     }
     XDIT_TRY(check_no_overlap(sl, so));
+    int splits = 1;
+    XDIT_TRY(resolve_splits(fn, sa, dtype, batch, q_len, seq_len, heads, head_dim, &splits));
+    if (splits > 1) {
+        const Span sw{sa.workspace, split_ws_bytes(batch, q_len, heads, head_dim, es, splits), "workspace"};
+        for (const Span* s : {&sb, &sk, &sv, &sq, &so, &sl}) XDIT_TRY(check_no_overlap(sw, *s));
+    }
     if (batch == 0 || heads == 0) return XDIT_OK;
 
     const int64_t plane = batch * seq_len * row;
@@ -277,6 +384,7 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
     p.len0 = (int)len[0];
     p.off1 = (int)off[1];
     p.len1 = (int)len[1];
+    if (splits > 1) return hip_status(launch_split(p, splits, sa.workspace, dtype), fn);
     const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
                                             : xdit::launch_attn_f32(p, g_stream);
     return hip_status(e, fn);
@@ -303,6 +411,46 @@ int xdit_patch_attn_ranges(const void* q, int64_t q_len, void* kv_buf, int32_t n
     return patch_ranges_impl("xdit_patch_attn_ranges", q, q_len, kv_buf, n_ranges, range_off,
                              range_len, fresh_k, fresh_v, out, lse, batch, seq_len, heads, head_dim,
                              dtype);
+}
+
+int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                                   int64_t head_dim, int32_t dtype, int32_t splits) {
+    clear_error();
+    if (check_dtype_dim(dtype, head_dim) != XDIT_OK) return -1;
+    if (check_dims("xdit_split_workspace_bytes", batch, q_len, kv_len, heads) != XDIT_OK) return -1;
+    if (splits > XDIT_MAX_SPLITS) return -1;
+    int s = splits;
+    if (dtype != XDIT_BF16) s = 1;
+    if (s <= 0) s = pick_splits((q_len + kSplitRows - 1) / kSplitRows * batch * heads, (kv_len + 127) / 128);
+    return s > 1 ? split_ws_bytes(batch, q_len, heads, head_dim, esize_of(dtype), s) : 0;
+}
+
+int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out, float* lse,
+                          int32_t splits, void* workspace, int64_t workspace_bytes, int64_t batch,
+                          int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
+                          int32_t dtype) {
+    clear_error();
+    SplitArgs sa;
+    sa.splits = splits;
+    sa.workspace = workspace;
+    sa.workspace_bytes = workspace_bytes;
+    return chunk_impl("xdit_chunk_attn_split", q, k, v, out, lse, batch, q_len, kv_len, heads,
+                      head_dim, dtype, 0, sa);
+}
+
+int xdit_patch_attn_split(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
+                          const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
+                          const void* fresh_v, void* out, float* lse, int32_t splits,
+                          void* workspace, int64_t workspace_bytes, int64_t batch, int64_t seq_len,
+                          int64_t heads, int64_t head_dim, int32_t dtype) {
+    clear_error();
+    SplitArgs sa;
+    sa.splits = splits;
+    sa.workspace = workspace;
+    sa.workspace_bytes = workspace_bytes;
+    return patch_ranges_impl("xdit_patch_attn_split", q, q_len, kv_buf, n_ranges, range_off,
+                             range_len, fresh_k, fresh_v, out, lse, batch, seq_len, heads,
+                             head_dim, dtype, sa);
 }
 
 int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const void* fresh_k,

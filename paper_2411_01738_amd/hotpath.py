@@ -18,13 +18,16 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (xdit_chunk_attn, xdit_chunk_attn_accum, xdit_lse_merge, xdit_patch_attn,
-               xdit_patch_attn_ranges)
+from . import (split_workspace_bytes, xdit_chunk_attn, xdit_chunk_attn_accum,
+               xdit_chunk_attn_split, xdit_lse_merge, xdit_patch_attn, xdit_patch_attn_ranges,
+               xdit_patch_attn_split)
 from .inputs import Tensors, Workload
 
 
 class HotPath:
-    def __init__(self, w: Workload, t: Tensors, device: str = "cuda"):
+    def __init__(self, w: Workload, t: Tensors, device: str = "cuda", split: bool = True):
+        """split: let the library split each query tile's keys over several
+        workgroups where one workgroup per query tile would leave CUs idle."""
         import torch
 
         self.w = w
@@ -63,6 +66,21 @@ class HotPath:
                                                       dtype=torch.float32))
             self.sp_out = torch.empty((B, nq, H, d), device=device, dtype=dt)
             self.sp_lse = torch.empty((B, H, nq), device=device, dtype=torch.float32)
+        # key-split workspace: the largest any call of the step needs
+        need = 0
+        self.patch_split = [False] * len(self.calls)
+        self.chunk_split = False
+        if split:
+            for p in range(len(self.calls)):
+                n = split_workspace_bytes(self.patch_q[p], w.N)
+                self.patch_split[p] = n > 0
+                need = max(need, n)
+            if self.sp_q is not None and not w.sp_ring:
+                for s_, e_ in w.sp_chunks:
+                    n = split_workspace_bytes(self.sp_q, e_ - s_)
+                    self.chunk_split = self.chunk_split or n > 0
+                    need = max(need, n)
+        self.workspace = torch.empty(need, device=device, dtype=torch.uint8) if need else None
 
     # -- calls ---------------------------------------------------------------
     def reset_buffer(self) -> None:
@@ -70,7 +88,10 @@ class HotPath:
 
     def patch_step(self, p: int) -> None:
         ranges, qrows = self.calls[p]
-        if len(ranges) == 1 and len(qrows) == ranges[0][1]:
+        if self.patch_split[p]:
+            xdit_patch_attn_split(self.patch_q[p], self.kv_buf, ranges, self.patch_k[p],
+                                  self.patch_v[p], self.patch_out[p], None, 0, self.workspace)
+        elif len(ranges) == 1 and len(qrows) == ranges[0][1]:
             off, ln = ranges[0]
             xdit_patch_attn(self.patch_q[p], self.kv_buf, off, ln, self.patch_k[p],
                             self.patch_v[p], self.patch_out[p])
@@ -84,6 +105,9 @@ class HotPath:
             # others are merged into it
             f = xdit_chunk_attn if r == 0 else xdit_chunk_attn_accum
             f(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.sp_out, self.sp_lse)
+        elif self.chunk_split:
+            xdit_chunk_attn_split(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
+                                  self.chunk_lse[r], 0, self.workspace)
         else:
             xdit_chunk_attn(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
                             self.chunk_lse[r])

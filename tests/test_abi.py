@@ -28,7 +28,8 @@ def header_functions():
 def test_header_declares_the_entry_points():
     names = header_functions()
     for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
-               "xdit_chunk_attn_accum", "xdit_lse_merge", "xdit_kv_update", "xdit_set_stream",
+               "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
+               "xdit_split_workspace_bytes", "xdit_lse_merge", "xdit_kv_update", "xdit_set_stream",
                "xdit_get_stream", "xdit_last_error", "xdit_version"]:
         assert fn in names
 
@@ -145,6 +146,43 @@ def test_ranges_rejections(ranges, q_len, fk, out, lse, code):
     assert lib.xdit_patch_attn_ranges(P(0), q_len, P(1), n, offs, lens, fk, P(3), out, lse,
                                       1, 16, 2, 64, 0) == code
     assert lib.xdit_last_error().decode(), "no message for a rejected call"
+
+
+def test_split_workspace_bytes():
+    lib = _lib.lib()
+    # sd3 patch step: 512 queries, 4429 keys, 2 x 24 heads of 64
+    o = 4 * 2 * 512 * 24 * 64 * 2
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 4) == o + 4 * 2 * 24 * 512 * 4
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 1) == 0
+    # by choice: 192 query tiles keep one round either way -> no split; a
+    # decode-like call (1 x 8 query tiles over 256 key tiles) takes 16
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 0) == 0
+    o16 = 16 * 64 * 8 * 128 * 2
+    assert lib.xdit_split_workspace_bytes(1, 64, 32768, 8, 128, 0, 0) == o16 + 16 * 8 * 64 * 4
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 1, 4) == 0  # float32: unsplit
+    # a launch that already fills the CUs (pixart patch: 256 query tiles) is not split
+    assert lib.xdit_split_workspace_bytes(2, 1024, 4096, 16, 72, 0, 0) == 0
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 17) == -1
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 80, 0, 2) == -1
+
+
+@needs_no_gpu
+def test_split_rejections():
+    lib = _lib.lib()
+    need = lib.xdit_split_workspace_bytes(1, 16, 1024, 2, 64, 0, 4)
+    assert lib.xdit_chunk_attn_split(P(0), P(1), P(2), P(3), P(4), 17, P(5), need,
+                                     1, 16, 1024, 2, 64, 0) == -4
+    assert lib.xdit_chunk_attn_split(P(0), P(1), P(2), P(3), P(4), 4, P(5), need - 1,
+                                     1, 16, 1024, 2, 64, 0) == -4
+    assert lib.xdit_chunk_attn_split(P(0), P(1), P(2), P(3), P(4), 4, None, 0,
+                                     1, 16, 1024, 2, 64, 0) == -4
+    assert lib.xdit_chunk_attn_split(P(0), P(1), P(2), P(3), P(4), 4, P(5) + 16, need,
+                                     1, 16, 1024, 2, 64, 0) == -5
+    assert lib.xdit_chunk_attn_split(P(0), P(1), P(2), P(3), P(4), 4, P(3), need,
+                                     1, 16, 1024, 2, 64, 0) == -6
+    n, offs, lens = _ranges((0, 8))
+    assert lib.xdit_patch_attn_split(P(0), 8, P(1), n, offs, lens, P(2), P(3), P(4), None, 4,
+                                     P(1) + 4096, need, 1, 1024, 2, 64, 0) == -6
 
 
 @needs_no_gpu

@@ -472,3 +472,69 @@ def test_ring_accum_continues_chunk_attn(orc, torch):
     ref_o, ref_l = orc.attention(q, k, v)
     check_out(to_np(out), ref_o, "bf16", "chunk then accum out")
     check_lse(lse.cpu().numpy(), ref_l, "bf16", "chunk then accum lse")
+
+
+# ---------------------------------------------------------------------------
+# Key-split forms
+# ---------------------------------------------------------------------------
+def _workspace(torch, nbytes):
+    return torch.empty(max(nbytes, 1), device="cuda", dtype=torch.uint8)
+
+
+@pytest.mark.parametrize("d,splits,Nk", [(64, 2, 1000), (72, 3, 777), (128, 4, 600), (64, 16, 700),
+                                         (72, 0, 2000), (128, 0, 1300)])
+def test_chunk_split(orc, torch, d, splits, Nk):
+    """Split sweeps merged by log-sum-exp equal attention over all keys; 16
+    splits over fewer tiles leave some parts empty."""
+    B, Nq, H = 1, 200, 3
+    q = random_io((B, Nq, H, d), "bf16", 400 + d)
+    k = random_io((B, Nk, H, d), "bf16", 401 + d)
+    v = random_io((B, Nk, H, d), "bf16", 402 + d)
+    qg = to_gpu(q, "bf16")
+    ws = _workspace(torch, xd.split_workspace_bytes(qg, Nk, splits))
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = torch.empty((B, H, Nq), device="cuda", dtype=torch.float32)
+    xd.xdit_chunk_attn_split(qg, to_gpu(k, "bf16"), to_gpu(v, "bf16"), out, lse, splits, ws)
+    torch.cuda.synchronize()
+    ref_o, ref_l = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, "bf16", f"split {splits} out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", f"split {splits} lse")
+
+
+@pytest.mark.parametrize("splits", [2, 4, 0])
+def test_patch_split(orc, torch, splits):
+    """The key-split patch step stores the fresh rows once and equals the
+    oracle's ranged step (in-context form: patch 0 plus the text rows)."""
+    B, N, H, d = 2, 900, 2, 64
+    ranges = [(0, 160), (800, 100)]
+    q = random_io((B, N, H, d), "bf16", 410)
+    kf = random_io((B, N, H, d), "bf16", 411)
+    vf = random_io((B, N, H, d), "bf16", 412)
+    kv_ref = np.ascontiguousarray(np.stack([random_io((B, N, H, d), "bf16", 413),
+                                            random_io((B, N, H, d), "bf16", 414)]))
+    kv = to_gpu(kv_ref, "bf16")
+    rows = _range_rows(ranges)
+    qs, fks, fvs = q[:, rows].copy(), kf[:, rows].copy(), vf[:, rows].copy()
+    ref_o, ref_l = orc.patch_ranges(qs, kv_ref, ranges, fks, fvs)
+    qg = to_gpu(qs, "bf16")
+    ws = _workspace(torch, xd.split_workspace_bytes(qg, N, splits))
+    out = _empty_out(torch, B, len(rows), H, d, "bf16")
+    lse = torch.empty((B, H, len(rows)), device="cuda", dtype=torch.float32)
+    xd.xdit_patch_attn_split(qg, kv, ranges, to_gpu(fks, "bf16"), to_gpu(fvs, "bf16"), out, lse,
+                             splits, ws)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, "bf16", f"patch split {splits} out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", f"patch split {splits} lse")
+    assert np.array_equal(to_np(kv), kv_ref), "split patch: buffer not bit-exact"
+
+
+def test_split_float32_runs_unsplit(orc, torch):
+    B, Nq, Nk, H, d = 1, 100, 500, 2, 64
+    q = random_io((B, Nq, H, d), "f32", 420)
+    k = random_io((B, Nk, H, d), "f32", 421)
+    v = random_io((B, Nk, H, d), "f32", 422)
+    out = _empty_out(torch, B, Nq, H, d, "f32")
+    xd.xdit_chunk_attn_split(to_gpu(q, "f32"), to_gpu(k, "f32"), to_gpu(v, "f32"), out, None, 4, None)
+    torch.cuda.synchronize()
+    ref_o, _ = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, "f32", "float32 split out")
