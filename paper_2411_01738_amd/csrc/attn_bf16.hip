@@ -96,6 +96,8 @@ struct Cfg {
     static constexpr int DMA_PER_TILE = TILE_BYTES / 1024;  // 64 lanes x 16 bytes per load
     static constexpr int DMA_PER_WAVE = (DMA_PER_TILE + NW - 1) / NW;
     static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
+    static constexpr int Q_PIECES = BM * ROWB / 1024;  // 64-lane loads of the query tile
+    static constexpr int Q_PER_WAVE = (Q_PIECES + NW - 1) / NW;
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = DV > D;      // a padding row of V^T holds ones
@@ -109,6 +111,7 @@ struct Cfg {
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
     static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads");
     static_assert(DMA_PER_TILE >= NW, "every wave loads part of each tile");
+    static_assert(BM * ROWB % 1024 == 0 && BM * ROWB <= CONST_OFF, "the query tile fits a stage's tiles");
     static_assert(LDS_BYTES <= kLdsBytes, "LDS budget");
 };
 
@@ -124,6 +127,7 @@ struct Args {
     float* lse;
     int B, H, Nq, Nk, q_tiles;
     int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
+    int sa0, sn0, sa1, sn1;      // tiles [sa, sa + sn) hold rows of fresh range 0 / 1
     float c2;  // softmax scale * log2(e)
     int accum;  // merge into the running (out, lse) instead of overwriting them
     // key splits: split sp of a query tile sweeps K/V tiles [T*sp/S, T*(sp+1)/S)
@@ -247,8 +251,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const int F = a.len0 + a.len1;  // fresh rows
     const uint16_t* fkbase = PATCH ? a.fk + (int64_t)b * F * a.H * D + headoff : nullptr;
     const uint16_t* fvbase = PATCH ? a.fv + (int64_t)b * F * a.H * D + headoff : nullptr;
+    // rows row0 .. rows-1 (none if row0 >= rows)
     auto rows_rsrc = [&](const uint16_t* base, int row0, int rows) -> Rsrc {
-        return rsrc(base + (int64_t)row0 * a.H * D, (uint32_t)(rows - row0) * rowb - headb);
+        return rsrc(base + (int64_t)row0 * a.H * D, rows > row0 ? (uint32_t)(rows - row0) * rowb - headb : 0u);
     };
 
     auto stage = [&](int s) -> unsigned char* { return lds + s * C::STAGE_BYTES; };
@@ -262,99 +267,50 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             (tid & 1) ? u32x4{0x3f80u, 0, 0, 0} : u32x4{0, 0, 0, 0};
     }
 
-    // The wave's 32 query rows as B operands (lane: query c, dims
-    // 16kk+8hf..+7), held in registers for the whole sweep.
+    // The query tile goes to LDS stage NST-1, which no K/V tile uses
+    // before iteration 0, in the same load stream as the tiles (issued
+    // first, so the wait for tile 0 covers it); rows past Nq read as zero.
+    // Routing it through LDS leaves no register with a vector-memory load
+    // outstanding, so the compiler never has to wait on one in the loop.
     const int qrow = qt * C::BM + qb * 32 + c;
     const bool qvalid = qrow < a.Nq;
-    const Rsrc rq = rsrc(a.q + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
     const Rsrc ro = rsrc(out_base + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
-    bf16x8 qf[C::KSTEPS];
+    {
+        const Rsrc rq = rows_rsrc(a.q + (int64_t)b * a.Nq * a.H * D + headoff, qt * C::BM, a.Nq);
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int col = 16 * kk + 8 * hf;
-        const uint32_t o = (qvalid && col < D) ? (uint32_t)qrow * rowb + headb + 2 * col : kOOB;
-        qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, o));
-    }
-    // Patch mode: this workgroup's share of the fresh rows goes into the
-    // buffer (all query tiles of a (batch, head) split the rows).  Nobody
-    // reads the fresh ranges of the buffer: they are taken from the fresh
-    // rows.
-    if constexpr (PATCH) {
-        const int share = qt * a.splits + sp, shares = a.q_tiles * a.splits;
-        const int r0 = (int)((int64_t)F * share / shares);
-        const int r1 = (int)((int64_t)F * (share + 1) / shares);
-        const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
-        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), 0, a.Nk);
-        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), 0, a.Nk);
-        // batches of U chunks per lane: all loads first, then all stores;
-        // chunks past the share use the out-of-range offset (reads give
-        // zero, writes are dropped)
-        constexpr int U = 4;
-        const int nchunks = (r1 - r0) * C::CH;
-        for (int e0 = 0; e0 < nchunks; e0 += U * NT) {
-            uint32_t cs[U], cd[U];
-            u32x4 ck[U], cv[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + tid + u * NT;
-                const int fr = r0 + e / C::CH, cc = 16 * (e % C::CH);
-                const int j = fr < a.len0 ? a.off0 + fr : a.off1 + fr - a.len0;  // buffer row
-                cs[u] = e < nchunks ? (uint32_t)fr * rowb + cc : kOOB;
-                cd[u] = e < nchunks ? (uint32_t)j * rowb + cc : kOOB;
-                ck[u] = bload(fk, cs[u]);
-                cv[u] = bload(fv, cs[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                bstore(wk, cd[u], ck[u]);
-                bstore(wv, cd[u], cv[u]);
+        for (int n = 0; n < C::Q_PER_WAVE; ++n) {
+            const int ins = wave + n * C::NW;
+            if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
+                const int p = 64 * ins + lane;  // row p / CH, chunk p % CH of the query tile
+                dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)(p / C::CH) * rowb + 16 * (p % C::CH));
             }
         }
-        // no wait: the stores are older than every tile load, and vector
-        // memory operations of a wave complete in issue order, so the first
-        // tile wait below covers them
     }
-
+    // the wave's 32 query rows as B operands (lane: query c, dims
+    // 16kk+8hf..+7), read from LDS after the prologue and held in registers
+    // for the whole sweep
+    bf16x8 qf[C::KSTEPS];
     // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
     // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
-    // row p / CH, logical chunk (p % CH) ^ swizzle(row).  dma_row / dma_off
-    // are that row and its byte offset from the tile's first row.
-    int dma_row[C::DMA_PER_WAVE];
+    // row p / CH, logical chunk (p % CH) ^ swizzle(row).  dma_off is its
+    // byte offset from the tile's first row.
     uint32_t dma_off[C::DMA_PER_WAVE];
 #pragma unroll
     for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
         const int p = 64 * (wave + n * C::NW) + lane;
         const int r = p / C::CH, pc = p % C::CH;
-        dma_row[n] = r;
         dma_off[n] = (uint32_t)r * rowb + 16 * (pc ^ (r & C::SWZ_MASK));
     }
 
-    // Where a tile's rows come from (uniform across the workgroup): all from
-    // the buffer (or the chunk), all from one fresh range, or several sources.
-    enum { kBuf = 0, kFresh0 = 1, kFresh1 = 2, kMixed = 3 };
-    auto tile_kind = [&](int t) -> int {
-        if constexpr (!PATCH) return kBuf;
-        const int lo = t * BN, hi = min(lo + BN, a.Nk);
-        const bool x0 = a.len0 > 0 && lo < a.off0 + a.len0 && a.off0 < hi;
-        const bool x1 = a.len1 > 0 && lo < a.off1 + a.len1 && a.off1 < hi;
-        if (!x0 && !x1) return kBuf;
-        if (!x1 && a.off0 <= lo && hi <= a.off0 + a.len0) return kFresh0;
-        if (!x0 && a.off1 <= lo && hi <= a.off1 + a.len1) return kFresh1;
-        return kMixed;
-    };
-
-    // Issue the loads of K and V tile t into stage s.
+    // Issue the loads of K and V tile t into stage s.  Most tiles hold only
+    // buffer (or chunk) rows and take the short path; in a patch, the few
+    // tiles that hold fresh rows (ranges of tiles fixed by the host) find
+    // their sources on the long one.
     auto load_tile = [&](int t, int s) {
-        const int kind = tile_kind(tb + t), lo = (tb + t) * BN;
+        const int gt = tb + t, lo = gt * BN;
         unsigned char* kdst = stage(s);
         unsigned char* vdst = stage(s) + C::TILE_BYTES;
-        if (kind != kMixed) {
-            // fresh row of buffer row j: j - off0 in range 0, len0 + j - off1
-            // in range 1; each range's resource ends at its last fresh row
-            const int fbase = kind == kFresh0 ? -a.off0 : a.len0 - a.off1;
-            const int fend = kind == kFresh0 ? a.len0 : F;
-            const Rsrc rk = kind == kBuf ? rows_rsrc(kbase, lo, a.Nk) : rows_rsrc(fkbase, lo + fbase, fend);
-            const Rsrc rv = kind == kBuf ? rows_rsrc(vbase, lo, a.Nk) : rows_rsrc(fvbase, lo + fbase, fend);
+        auto issue = [&](Rsrc rk, Rsrc rv) {
 #pragma unroll
             for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
                 const int ins = wave + n * C::NW;
@@ -363,27 +319,46 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                     dma16(rv, vdst + 1024 * ins, dma_off[n]);
                 }
             }
-        } else {
-            // the tile straddles a range boundary (at most four per sweep):
-            // each lane loads its row from its own source
-            const Rsrc rk = rows_rsrc(kbase, lo, a.Nk), rv = rows_rsrc(vbase, lo, a.Nk);
-            const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
+        };
+        const bool plain = !PATCH || ((unsigned)(gt - a.sa0) >= (unsigned)a.sn0 &&
+                                      (unsigned)(gt - a.sa1) >= (unsigned)a.sn1);
+        if (__builtin_expect(plain, 1)) {
+            issue(rows_rsrc(kbase, lo, a.Nk), rows_rsrc(vbase, lo, a.Nk));
+            return;
+        }
+        // fresh row of buffer row j: j - off0 in range 0, len0 + j - off1 in
+        // range 1
+        const int hi = min(lo + BN, a.Nk);
+        const bool all0 = a.off0 <= lo && hi <= a.off0 + a.len0;
+        const bool all1 = a.off1 <= lo && hi <= a.off1 + a.len1;
+        if (all0 || all1) {
+            // every row from one fresh range; its resource ends at the
+            // range's last fresh row
+            const int fbase = all0 ? -a.off0 : a.len0 - a.off1;
+            const int fend = all0 ? a.len0 : F;
+            issue(rows_rsrc(fkbase, lo + fbase, fend), rows_rsrc(fvbase, lo + fbase, fend));
+            return;
+        }
+        // the tile straddles a range edge (at most four per sweep): each
+        // lane loads its row from its own source
+        const Rsrc rk = rows_rsrc(kbase, lo, a.Nk), rv = rows_rsrc(vbase, lo, a.Nk);
+        const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
 #pragma unroll
-            for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
-                const int ins = wave + n * C::NW;
-                if (C::DMA_PER_TILE % C::NW == 0 || ins < C::DMA_PER_TILE) {
-                    const int j = lo + dma_row[n];
-                    const bool in0 = (unsigned)(j - a.off0) < (unsigned)a.len0;
-                    const bool in1 = (unsigned)(j - a.off1) < (unsigned)a.len1;
-                    if (in0 || in1) {
-                        const int fr = in0 ? j - a.off0 : a.len0 + j - a.off1;
-                        const uint32_t o = dma_off[n] + (uint32_t)(fr - dma_row[n]) * rowb;
-                        dma16(fk, kdst + 1024 * ins, o);
-                        dma16(fv, vdst + 1024 * ins, o);
-                    } else {
-                        dma16(rk, kdst + 1024 * ins, dma_off[n]);
-                        dma16(rv, vdst + 1024 * ins, dma_off[n]);
-                    }
+        for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
+            const int ins = wave + n * C::NW;
+            if (C::DMA_PER_TILE % C::NW == 0 || ins < C::DMA_PER_TILE) {
+                const int r = (64 * ins + lane) / C::CH;  // row within the tile
+                const int j = lo + r;
+                const bool in0 = (unsigned)(j - a.off0) < (unsigned)a.len0;
+                const bool in1 = (unsigned)(j - a.off1) < (unsigned)a.len1;
+                if (in0 || in1) {
+                    const int fr = in0 ? j - a.off0 : a.len0 + j - a.off1;
+                    const uint32_t o = dma_off[n] + (uint32_t)(fr - r) * rowb;
+                    dma16(fk, kdst + 1024 * ins, o);
+                    dma16(fv, vdst + 1024 * ins, o);
+                } else {
+                    dma16(rk, kdst + 1024 * ins, dma_off[n]);
+                    dma16(rv, vdst + 1024 * ins, dma_off[n]);
                 }
             }
         }
@@ -580,25 +555,25 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     using T_ = std::true_type;
     using F_ = std::false_type;
 
+    // Prologue: the first NST-1 tiles load whether or not this sweep has
+    // that many (a tile past the sequence end reads zeros, one past this
+    // split's range lands in a stage nobody reads).
     f32x16 sA[NKB], sB[NKB];
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t) load_tile(t, t);
+    // tile 0 (and the query tile, loaded before it) must have landed, NST-2
+    // younger tiles may be in flight, and the constant chunks must be
+    // written before anyone reads them
+    wait_tiles(std::integral_constant<int, NST - 2>{});
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int kk = 0; kk < C::KSTEPS; ++kk) {
+        const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
+        qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + lc) : C::CONST_OFF));
+    }
     if (ntiles > 0) {
-#pragma unroll
-        for (int t = 0; t < NST - 1; ++t)
-            if (t < ntiles) load_tile(t, t);
-        // the query loads (issued first) complete while the tiles load; the
-        // loop body then never waits on memory operations other than tile
-        // loads
-#pragma unroll
-        for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" ::"v"(qf[kk]));
-        // tile 0 must have landed (up to NST-2 younger tiles may be in
-        // flight) and the constant chunks must be written before anyone
-        // reads them
-        if (NST >= 4 && ntiles >= 3) wait_tiles(std::integral_constant<int, 2>{});
-        else if (ntiles >= 2) wait_tiles(std::integral_constant<int, 1>{});
-        else wait_vmem<0>();
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
         qk(0, sA);
         mask(0, sA);
         update_max(row_max(sA));
@@ -620,7 +595,55 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     } else if (t + 1 == ntiles) {
         iteration(t, sA, sB, F_{}, F_{});
     }
-    __syncthreads();  // every wave is done with the stages
+    // Every wave is done with the stages, and no tile load is in flight
+    // (with fewer than NST-1 tiles the prologue's spare loads are still
+    // outstanding here; the key-split exchange below reuses their LDS).
+    wait_vmem<0>();
+    __syncthreads();
+
+    // Patch mode: this workgroup's share of the fresh rows goes into the
+    // buffer (the workgroups of a (batch, head) split the rows).  Nothing in
+    // this kernel reads the fresh ranges of the buffer: tiles take those rows
+    // from the fresh tensors.  The copy runs after the sweep, so its memory
+    // operations hold up none of the sweep's waits, and the first batch's
+    // loads are in flight during the key-split merge and the output.
+    constexpr int CU = 4;  // 16-byte chunks per lane and batch
+    const int cshare = qt * a.splits + sp, cshares = a.q_tiles * a.splits;
+    const int cr0 = (int)((int64_t)F * cshare / cshares);
+    const int cn = ((int)((int64_t)F * (cshare + 1) / cshares) - cr0) * C::CH;  // chunks of the share
+    uint32_t cd[CU];
+    u32x4 ck[CU], cv[CU];
+    // loads of batch e0 .. e0 + CU*NT - 1; chunks past the share use the
+    // out-of-range offset (reads give zero, writes are dropped)
+    auto copy_load = [&](int e0) {
+        const Rsrc fk = rows_rsrc(fkbase, 0, F), fv = rows_rsrc(fvbase, 0, F);
+#pragma unroll
+        for (int u = 0; u < CU; ++u) {
+            const int e = e0 + tid + u * NT;
+            const int fr = cr0 + e / C::CH, cc = 16 * (e % C::CH);
+            const int j = fr < a.len0 ? a.off0 + fr : a.off1 + fr - a.len0;  // buffer row
+            const uint32_t cs = e < cn ? (uint32_t)fr * rowb + cc : kOOB;
+            cd[u] = e < cn ? (uint32_t)j * rowb + cc : kOOB;
+            ck[u] = bload(fk, cs);
+            cv[u] = bload(fv, cs);
+        }
+    };
+    // stores of the loaded batch, then the remaining batches
+    auto copy_rest = [&]() {
+        const Rsrc wk = rows_rsrc(a.wk + (kbase - a.k), 0, a.Nk);
+        const Rsrc wv = rows_rsrc(a.wv + (vbase - a.v), 0, a.Nk);
+        for (int e0 = 0;;) {
+#pragma unroll
+            for (int u = 0; u < CU; ++u) {
+                bstore(wk, cd[u], ck[u]);
+                bstore(wv, cd[u], cv[u]);
+            }
+            e0 += CU * NT;
+            if (e0 >= cn) break;
+            copy_load(e0);
+        }
+    };
+    if constexpr (PATCH) copy_load(0);
 
     // Merge the KS partial sweeps of each query block.  Slots are lane-major
     // so the exchange is free of bank conflicts.
@@ -635,7 +658,10 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[db][i];
         }
-        __syncthreads();
+        // LDS only: a bare barrier, which leaves the copy loads in flight
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
         if (kh == 0) {
             float M = m_ref;
 #pragma unroll
@@ -660,7 +686,11 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             m_ref = M;
         }
     }
-    if (kh != 0) return;
+    static_assert(KS > 1, "key-split waves merge into those of split 0");
+    if (kh != 0) {
+        if constexpr (PATCH) copy_rest();
+        return;
+    }
 
     float l_tot;
     if constexpr (C::SUM_BY_MFMA) {
@@ -722,6 +752,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             }
         }
     if (lse_base && hf == 0 && qvalid) lse_base[lidx] = lse_out;
+    if constexpr (PATCH) copy_rest();
 }
 
 template <int D, int QB, int KS, int KW, bool PATCH>
@@ -745,6 +776,11 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.len0 = p.len0;
     a.off1 = p.off1;
     a.len1 = p.len1;
+    // tiles holding rows of each fresh range
+    a.sa0 = p.len0 > 0 ? p.off0 / C::BN : 0;
+    a.sn0 = p.len0 > 0 ? (p.off0 + p.len0 + C::BN - 1) / C::BN - a.sa0 : 0;
+    a.sa1 = p.len1 > 0 ? p.off1 / C::BN : 0;
+    a.sn1 = p.len1 > 0 ? (p.off1 + p.len1 + C::BN - 1) / C::BN - a.sa1 : 0;
     a.q_tiles = (p.Nq + C::BM - 1) / C::BM;
     a.splits = p.splits > 1 ? p.splits : 1;
     a.out_split = p.out_split;
