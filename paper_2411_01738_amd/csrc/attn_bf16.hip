@@ -85,8 +85,27 @@ struct Cfg {
     static constexpr int DBLK = DV / 32;
     static constexpr int CH = D / 8;                 // 16-byte chunks per K/V row
     static constexpr int ROWB = 16 * CH;             // bytes per row in LDS
-    static constexpr bool SWZ = (CH & (CH - 1)) == 0;  // XOR-swizzle chunks by row
-    static constexpr int SWZ_MASK = SWZ ? (CH < 8 ? CH - 1 : 7) : 0;
+    // LDS layout of a row: logical chunk c sits in slot c ^ swz(row).  Both
+    // this swizzle and the key order krow (PERM) are chosen so that the
+    // operand reads of a tile hit distinct banks (64 banks of 4 bytes; a
+    // 16-byte read serves 16 lanes per cycle, an 8-byte transposing read
+    // 32).  The V reads of the two half k-steps are E_ROWS rows apart, and
+    // those of successive k-steps 16: swz ignores both offsets.
+    //  d = 72 (9 chunks, rows 36 banks apart): no swizzle; krow puts the
+    //    four keys of a transposing read four rows apart.
+    //  d = 64 (8 chunks, two rows per bank cycle): rows in order; the
+    //    swizzle (bits 1 and 2 of the row) leaves the K reads 2-way and
+    //    makes the V reads conflict-free.
+    //  d = 128 (16 chunks, one row per bank cycle): krow as for d = 72 and
+    //    a swizzle of row bits 0, 2, 3: V reads conflict-free, K reads
+    //    2-way.
+    static constexpr bool PERM = CH != 8;
+    static constexpr int E_ROWS = PERM ? 2 : 8;  // rows between the two half k-steps
+    __device__ static constexpr int swz(int r) {
+        if constexpr (CH == 8) return (((r >> 1) & 1) << 2) | ((r >> 2) & 1);
+        else if constexpr (CH == 16) return (((r >> 2) & 3) << 2) | (r & 1);
+        else return 0;
+    }
     static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
     static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
@@ -193,6 +212,14 @@ __device__ __forceinline__ void lds_wait_all(u32x2 (&r)[NS][NB][2]) {
         for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(r[i][j][0]), "+v"(r[i][j][1]));
 }
 
+// Key of S^T row x (0..31) of a 32-key block: x = 16a + 8e + 4h + j is key
+// 16a + 4j + 2e + h when PERM, key x otherwise.
+template <bool PERM>
+__device__ __forceinline__ int krow(int x) {
+    if constexpr (PERM) return (x & 16) + 4 * (x & 3) + 2 * ((x >> 3) & 1) + ((x >> 2) & 1);
+    else return x;
+}
+
 __device__ __forceinline__ int xcd_remap(int pid, int total) {
     const int per = total >> 3, rem = total & 7;
     const int xcd = pid & 7, loc = pid >> 3;
@@ -281,8 +308,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         for (int n = 0; n < C::Q_PER_WAVE; ++n) {
             const int ins = wave + n * C::NW;
             if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
-                const int p = 64 * ins + lane;  // row p / CH, chunk p % CH of the query tile
-                dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)(p / C::CH) * rowb + 16 * (p % C::CH));
+                // slot p: row p / CH, logical chunk (p % CH) ^ swz(row)
+                const int p = 64 * ins + lane, r = p / C::CH;
+                dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
             }
         }
     }
@@ -299,7 +327,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
         const int p = 64 * (wave + n * C::NW) + lane;
         const int r = p / C::CH, pc = p % C::CH;
-        dma_off[n] = (uint32_t)r * rowb + 16 * (pc ^ (r & C::SWZ_MASK));
+        dma_off[n] = (uint32_t)r * rowb + 16 * (pc ^ C::swz(r));
     }
 
     // Issue the loads of K and V tile t into stage s.  Most tiles hold only
@@ -365,29 +393,30 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     };
 
     // LDS byte offsets (within a stage) of this lane's operand reads.
-    //  K (A operand of S^T): row kw0 + 32kb + c, logical chunk 2kk + hf;
-    //  chunks past d read the zero chunk.
+    //  K (A operand of S^T): row kw0 + 32kb + krow(c), logical chunk
+    //  2kk + hf; chunks past d read the zero chunk.
     //  V (A operand of O^T, transposed read from the V tile, which follows
-    //  the K tile in the stage): in each 16-lane group, lane
-    //  4j+q reads dims d0+4q..+3 of key kw0 + 16ks + 8e + 4hf + j, where
-    //  d0 = 32db + 16*(group & 1) and e = 0, 1 selects the half k-step;
-    //  lane i of the group then holds dim d0 + i of the four keys.  Padding
-    //  dims read the constant chunks (ones for dim d, zeros after it).
+    //  the K tile in the stage): in each 16-lane group, lane 4j+q reads dims
+    //  d0+4q..+3 of key kw0 + 16ks + krow(8e + 4hf + j), where d0 = 32db +
+    //  16*(group & 1) and e = 0, 1 selects the half k-step; lane i of the
+    //  group then holds dim d0 + i of the four keys, in the order of the
+    //  weights P (S^T rows).  Padding dims read the constant chunks (ones
+    //  for dim d, zeros after it).
     const int kw0 = kh * KW;  // this wave's first key within a tile
     uint32_t kaddr[C::KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int r = kw0 + c, lc = 2 * kk + hf;
-        kaddr[kk] = lc < C::CH ? r * C::ROWB + 16 * (lc ^ (r & C::SWZ_MASK)) : C::CONST_OFF;
+        const int r = kw0 + krow<C::PERM>(c), lc = 2 * kk + hf;
+        kaddr[kk] = lc < C::CH ? r * C::ROWB + 16 * (lc ^ C::swz(r)) : C::CONST_OFF;
     }
     const int gi = lane & 15, grp = lane >> 4;
-    const int vkey0 = kw0 + 4 * hf + (gi >> 2);
+    const int vkey0 = kw0 + krow<C::PERM>(4 * hf + (gi >> 2));
     uint32_t vaddr[C::DBLK];
 #pragma unroll
     for (int db = 0; db < C::DBLK; ++db) {
         const int dim = 32 * db + 16 * (grp & 1) + 4 * (gi & 3);
         if (dim < D)
-            vaddr[db] = C::TILE_BYTES + vkey0 * C::ROWB + 16 * ((dim >> 3) ^ (vkey0 & C::SWZ_MASK)) + 2 * (dim & 7);
+            vaddr[db] = C::TILE_BYTES + vkey0 * C::ROWB + 16 * ((dim >> 3) ^ C::swz(vkey0)) + 2 * (dim & 7);
         else
             vaddr[db] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
     }
@@ -401,7 +430,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const float thr = kRescaleLog2 / a.c2;
 
     // S^T of tile t for this wave's KW keys x 32 queries: s[kb][i] = score of
-    // key kw0 + 32kb + 8(i/4) + 4hf + (i%4) of the tile against query c.
+    // key kw0 + 32kb + krow(8(i/4) + 4hf + (i%4)) of the tile against query c.
     auto qk = [&](int t, f32x16 (&s)[NKB]) {
         const unsigned char* st = stage(t % NST);
 #pragma unroll
@@ -423,7 +452,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int key = (tb + t) * BN + kw0 + 32 * kb + 8 * (i >> 2) + 4 * hf + (i & 3);
+                    const int key = (tb + t) * BN + kw0 + 32 * kb + krow<C::PERM>(8 * (i >> 2) + 4 * hf + (i & 3));
                     if (key >= a.Nk) s[kb][i] = -INFINITY;
                 }
         }
@@ -480,12 +509,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                     // block with padding dims: their lanes keep reading the constant chunk
                     const bool cst = vaddr[db] >= (uint32_t)C::CONST_OFF;
                     const uint32_t a0 = vst + vaddr[db] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
-                    const uint32_t a1 = vst + vaddr[db] + (cst ? 0u : (uint32_t)((16 * ks + 8) * C::ROWB));
+                    const uint32_t a1 = vst + vaddr[db] + (cst ? 0u : (uint32_t)((16 * ks + C::E_ROWS) * C::ROWB));
                     vr[ks][db][0] = tr_read<0>(a0);
                     vr[ks][db][1] = tr_read<0>(a1);
                 } else {
                     vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db]);
-                    vr[ks][db][1] = tr_read<(16 * ks + 8) * C::ROWB>(vst + vaddr[db]);
+                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB>(vst + vaddr[db]);
                 }
             });
         });
@@ -571,7 +600,7 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
         const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
-        qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + lc) : C::CONST_OFF));
+        qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
     }
     if (ntiles > 0) {
         qk(0, sA);
