@@ -93,19 +93,20 @@ struct Cfg {
     // those of successive k-steps 16: swz ignores both offsets.
     //  d = 72 (9 chunks, rows 36 banks apart): no swizzle; krow puts the
     //    four keys of a transposing read four rows apart.
-    //  d = 64 (8 chunks, two rows per bank cycle): rows in order; the
-    //    swizzle (bits 1 and 2 of the row) leaves the K reads 2-way and
-    //    makes the V reads conflict-free.
-    //  d = 128 (16 chunks, one row per bank cycle): krow as for d = 72 and
-    //    a swizzle of row bits 0, 2, 3: V reads conflict-free, K reads
-    //    2-way.
+    //  d = 64 (8 chunks, two rows per bank cycle): rows in order, swizzle
+    //    of row bits 1..3.
+    //  d = 128 (16 chunks, one row per bank cycle): krow as for d = 72,
+    //    swizzle of row bits 0..3.
+    // Where the swizzle differs between the two half k-steps (E_SPLIT),
+    // each has its own V read address.
     static constexpr bool PERM = CH != 8;
     static constexpr int E_ROWS = PERM ? 2 : 8;  // rows between the two half k-steps
     __device__ static constexpr int swz(int r) {
-        if constexpr (CH == 8) return (((r >> 1) & 1) << 2) | ((r >> 2) & 1);
-        else if constexpr (CH == 16) return (((r >> 2) & 3) << 2) | (r & 1);
+        if constexpr (CH == 8) return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+        else if constexpr (CH == 16) return r & 15;
         else return 0;
     }
+    static constexpr bool E_SPLIT = CH == 8 || CH == 16;
     static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
     static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
@@ -411,14 +412,18 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     }
     const int gi = lane & 15, grp = lane >> 4;
     const int vkey0 = kw0 + krow<C::PERM>(4 * hf + (gi >> 2));
-    uint32_t vaddr[C::DBLK];
+    constexpr int NE = C::E_SPLIT ? 2 : 1;
+    uint32_t vaddr[C::DBLK][NE];
 #pragma unroll
     for (int db = 0; db < C::DBLK; ++db) {
         const int dim = 32 * db + 16 * (grp & 1) + 4 * (gi & 3);
         if (dim < D)
-            vaddr[db] = C::TILE_BYTES + vkey0 * C::ROWB + 16 * ((dim >> 3) ^ C::swz(vkey0)) + 2 * (dim & 7);
+            for (int e = 0; e < NE; ++e) {
+                const int r = vkey0 + C::E_ROWS * e;
+                vaddr[db][e] = C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7);
+            }
         else
-            vaddr[db] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
+            for (int e = 0; e < NE; ++e) vaddr[db][e] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
     }
 
     f32x16 oacc[C::DBLK];
@@ -507,14 +512,18 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 constexpr int db = decltype(dbc)::value;
                 if constexpr (32 * db + 31 >= D && C::DV > D) {
                     // block with padding dims: their lanes keep reading the constant chunk
-                    const bool cst = vaddr[db] >= (uint32_t)C::CONST_OFF;
-                    const uint32_t a0 = vst + vaddr[db] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
-                    const uint32_t a1 = vst + vaddr[db] + (cst ? 0u : (uint32_t)((16 * ks + C::E_ROWS) * C::ROWB));
+                    static_assert(!C::E_SPLIT, "padding dims only with one V address per block");
+                    const bool cst = vaddr[db][0] >= (uint32_t)C::CONST_OFF;
+                    const uint32_t a0 = vst + vaddr[db][0] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
+                    const uint32_t a1 = vst + vaddr[db][0] + (cst ? 0u : (uint32_t)((16 * ks + C::E_ROWS) * C::ROWB));
                     vr[ks][db][0] = tr_read<0>(a0);
                     vr[ks][db][1] = tr_read<0>(a1);
+                } else if constexpr (C::E_SPLIT) {
+                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
+                    vr[ks][db][1] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][NE - 1]);
                 } else {
-                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db]);
-                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB>(vst + vaddr[db]);
+                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
+                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB>(vst + vaddr[db][0]);
                 }
             });
         });
