@@ -38,13 +38,14 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # HBM traffic per launch of the dominant kernel, in bytes: rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE (KiB per dispatch, one counter per run), scaled by
 # what the same counters read for kv_update_kernel copying a known size
-# (FETCH x 1.9944, WRITE x 1.0).  Each entry holds the sha256 prefix of the
+# (FETCH x about 1.995, WRITE x 1.0).  Each entry holds the sha256 prefix of the
 # kernel source it was taken on; a different source reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (51597 + 13845) * 1024, "src": "52e15906ea183741"},
-    ("sd3", "patch_attn"): {"bytes": (59291 + 9216) * 1024, "src": "52e15906ea183741"},
-    ("flux", "chunk_attn"): {"bytes": (116118 + 25747) * 1024, "src": "52e15906ea183741"},
-    ("cog", "patch_attn"): {"bytes": (265506 + 19744) * 1024, "src": "52e15906ea183741"},
+    ("pixart", "patch_attn"): {"bytes": (50079 + 17969) * 1024, "src": "6c73b0e0cb1a65a1"},
+    ("sd3", "patch_attn"): {"bytes": (59043 + 9216) * 1024, "src": "6c73b0e0cb1a65a1"},
+    ("flux", "chunk_attn"): {"bytes": (115847 + 25746) * 1024, "src": "6c73b0e0cb1a65a1"},
+    ("flux_ring", "chunk_attn"): {"bytes": (135471 + 25771) * 1024, "src": "6c73b0e0cb1a65a1"},
+    ("cog", "chunk_attn"): {"bytes": (133433 + 109989) * 1024, "src": "6c73b0e0cb1a65a1"},
 }
 
 
@@ -66,7 +67,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="pixart",
-                    choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "pixart_hybrid",
+                    choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "sd3_ic_bal", "pixart_hybrid",
                              "flux_ring"])
     ap.add_argument("--no-split", action="store_true",
                     help="never split a query tile's keys over several workgroups")
@@ -336,6 +337,9 @@ def main():
                    " steps + 8-chunk split (Q all rows) + merge",
             "sd3_ic": "sd3-1024px in-context: B=2 H=24 d=64, 4096 image + 333 text tokens,"
                       " M=8 patch steps, patch 0 carries the text (845 fresh rows and queries)",
+            "sd3_ic_bal": "sd3-1024px in-context, balanced partition: B=2 H=24 d=64, 4096 image"
+                          " + 333 text tokens, M=8 patch steps of 553-554 fresh rows (patch 0:"
+                          " 220 image + 333 text)",
             "flux_ring": "flux-2048px SP share, ring form: B=1 H=24 d=128, Q 4224 rows, 4 chunks"
                          " of 4224 each merged into the running output as it arrives",
             "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"

@@ -36,6 +36,8 @@ class Workload:
     sp_chunks: tuple = ()  # ((start, stop), ...) K/V row ranges, one per chunk
     # PipeFusion variants (Sections 4.1.2 and 4.1.4)
     in_context: bool = False  # the text rows travel with patch 0
+    balanced: bool = False    # with in_context: patch 0 takes fewer image rows, so
+                              # that every patch step refreshes about as many rows
     sp_degree: int = 1        # hybrid SP x PipeFusion: this GPU's queries are the
                               # first 1/sp_degree of each patch step's query rows
     sp_ring: bool = False     # SP chunks merged into a running (out, lse) one by one
@@ -47,14 +49,24 @@ class Workload:
         return self.n_img + self.n_txt
 
     def patches(self):
-        """(offset, length) of the M patches: near-equal contiguous splits of
-        the image rows, the first (n_img mod M) patches one row longer."""
+        """(offset, length) of the M patches: contiguous splits of the image
+        rows, near-equal (the first n_img mod M one row longer), or, for
+        a balanced in-context partition, patch 0 cut to about
+        (n_img + n_txt) / M - n_txt rows and the rest split near-equally
+        over the other patches, so that patch 0 with the text rows is no
+        longer than the others."""
         if self.M == 0:
             return []
-        base, extra = divmod(self.n_img, self.M)
+        lens = []
+        if self.in_context and self.balanced and self.M > 1:
+            first = max(0, min(self.n_img, (self.n_img + self.n_txt) // self.M - self.n_txt))
+            base, extra = divmod(self.n_img - first, self.M - 1)
+            lens = [first] + [base + (1 if p < extra else 0) for p in range(self.M - 1)]
+        else:
+            base, extra = divmod(self.n_img, self.M)
+            lens = [base + (1 if p < extra else 0) for p in range(self.M)]
         out, off = [], 0
-        for p in range(self.M):
-            ln = base + (1 if p < extra else 0)
+        for ln in lens:
             out.append((off, ln))
             off += ln
         return out
@@ -106,6 +118,10 @@ WORKLOADS = {
     "sd3_ic": Workload("sd3_ic", "bf16", 2, 24, 64, 4096, 333, 8, 2, in_context=True,
                        note="SD3 with in-context conditioning: the 333 text tokens travel"
                             " with patch 0"),
+    "sd3_ic_bal": Workload("sd3_ic_bal", "bf16", 2, 24, 64, 4096, 333, 8, 2, in_context=True,
+                           balanced=True,
+                           note="SD3 with in-context conditioning and a load-balanced image"
+                                " partition: patch 0 takes 220 image rows + the 333 text rows"),
     "pixart_hybrid": Workload("pixart_hybrid", "bf16", 2, 16, 72, 4096, 0, 4, 1, sp_degree=2,
                               note="Pixart 1024px, PipeFusion x 2-way sequence parallelism:"
                                    " gathered fresh K/V, this GPU's half of each patch's"

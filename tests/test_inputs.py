@@ -53,3 +53,18 @@ def test_workload_geometry():
     assert all(r == [(1024 * p, 1024)] and list(q) == list(range(1024 * p, 1024 * p + 512))
                for p, (r, q) in enumerate(hy))
     assert [len(q) for _, q in WORKLOADS["cog"].patch_calls()] == lens
+
+
+def test_balanced_in_context_partition():
+    """With the text rows riding with patch 0, the balanced partition gives
+    patch 0 fewer image rows so that every patch step refreshes about
+    (n_img + n_txt) / M rows; the patches still tile the image rows."""
+    w = WORKLOADS["sd3_ic_bal"]
+    pt = w.patches()
+    assert sum(ln for _, ln in pt) == w.n_img
+    assert all(pt[i + 1][0] == pt[i][0] + pt[i][1] for i in range(len(pt) - 1)) and pt[0][0] == 0
+    sizes = [len(q) for _, q in w.patch_calls()]
+    assert sum(sizes) == w.n_img + w.n_txt
+    assert max(sizes) - min(sizes) <= 1
+    assert pt[0][1] == (w.n_img + w.n_txt) // w.M - w.n_txt == 220
+    assert w.patch_calls()[0][0] == [(0, 220), (4096, 333)]

@@ -24,7 +24,7 @@ def _rows(w, n: int, target: int, extra=()):
     return sample_rows(n, step, edges)
 
 
-@pytest.mark.parametrize("name", ["tiny", "pixart", "sd3", "cog", "sd3_ic", "pixart_hybrid"])
+@pytest.mark.parametrize("name", ["tiny", "pixart", "sd3", "cog", "sd3_ic", "sd3_ic_bal", "pixart_hybrid"])
 def test_patch_steps_full_size(name):
     torch = torch_mod()
     orc = oracle.get()
