@@ -15,6 +15,9 @@ and marshals numpy arrays.  Definitions (see the C file for the formulas):
                   serial one)
 * ``patch``       PipeFusion patch step over a fresh/stale K/V buffer
                   (Section 4.1.2; Section 4.1.4 for the buffer contents)
+* ``stage_step``  one stage micro-step at one attention layer: QKV
+                  projections, the patch step, the output projection
+                  (Section 4.1.2; Section 3 on the projections)
 
 Layouts: activations [B, N, H, d]; K/V buffer [2, B, N, H, d]; LSE [B, H, Nq].
 Inputs are float32 arrays holding the exact values given to the GPU (bf16
@@ -68,6 +71,11 @@ class Oracle:
         lib.xo_patch_ranges.argtypes = [_f32p, _i64, _f32p, ctypes.c_int32, ctypes.c_void_p,
                                         ctypes.c_void_p, _f32p, _f32p, _i64, _i64, _i64, _i64,
                                         ctypes.c_void_p, _i64, _f64p, ctypes.c_void_p]
+        lib.xo_stage.restype = ctypes.c_int
+        lib.xo_stage.argtypes = [_f32p, _f32p, _f32p, _f32p, _f32p, _f32p, _i64, _i64, _i64, _i64,
+                                 _i64, _i64, _i64, ctypes.c_void_p, _i64, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p]
         lib.xo_num_threads.restype = ctypes.c_int
         lib.xo_set_num_threads.argtypes = [ctypes.c_int]
         self.lib = lib
@@ -201,6 +209,35 @@ class Oracle:
         if rc:
             raise ValueError("xo_patch_ranges rejected its arguments")
         return out, lse
+
+    def stage_step(self, x, wq, wk, wv, wo, kv_buf, off, rows=None):
+        """One PipeFusion stage micro-step at one attention layer: q/k/v =
+        x W{q,k,v} for the patch rows x [B,L,C] (W [C,H*d]), the patch step
+        over kv_buf [2,B,N,H,d] (float32, in place: rows [off, off+L) take k/v
+        rounded to float), y = o Wo (Wo [H*d,C]).  Returns a dict of float64
+        arrays: y [B,nrows,C], o [B,nrows,H,d], q/k/v [B,L,H,d]."""
+        if kv_buf.dtype != np.float32 or not kv_buf.flags.c_contiguous:
+            raise TypeError("kv_buf must be a C-contiguous float32 array")
+        x, wq, wk, wv, wo = (self._f32(a) for a in (x, wq, wk, wv, wo))
+        _, B, N, H, d = kv_buf.shape
+        L, C = x.shape[1], x.shape[2]
+        HD = H * d
+        if (x.shape[0] != B or wq.shape != (C, HD) or wk.shape != (C, HD) or wv.shape != (C, HD)
+                or wo.shape != (HD, C)):
+            raise ValueError("stage shapes mismatch")
+        if rows is None:
+            rows_ptr, nrows = None, L
+        else:
+            rows_arr = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+            rows_ptr, nrows = rows_arr.ctypes.data, rows_arr.size
+        res = {"y": np.zeros((B, nrows, C)), "o": np.zeros((B, nrows, H, d)),
+               "q": np.zeros((B, L, H, d)), "k": np.zeros((B, L, H, d)), "v": np.zeros((B, L, H, d))}
+        rc = self.lib.xo_stage(x, wq, wk, wv, wo, kv_buf, int(off), L, B, N, H, d, C, rows_ptr,
+                               nrows, res["y"].ctypes.data, res["o"].ctypes.data,
+                               res["q"].ctypes.data, res["k"].ctypes.data, res["v"].ctypes.data)
+        if rc:
+            raise ValueError("xo_stage rejected its arguments")
+        return res
 
 
 _default = None

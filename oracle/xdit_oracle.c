@@ -24,6 +24,9 @@
  *                  patch's queries attend over the whole buffer
  *                  (Section 4.1.2, PipeFusion; Section 4.1.4 on storing
  *                  communicated K/V into that buffer)
+ *   stage          one stage micro-step at one attention layer: QKV
+ *                  projections of the patch rows, the patch step, the output
+ *                  projection (Section 4.1.2; Section 3 on the projections)
  *
  * Layout (a reading: the paper does not fix one): activations are
  * sequence-major [B, N, H, d] with d contiguous; the K/V buffer is
@@ -250,4 +253,130 @@ int xo_patch_ranges(const float* q, int64_t Nq, float* kv_buf, int32_t nr, const
         base += lens[r];
     }
     return xo_attention(q, kv_buf, kv_buf + plane, B, Nq, N, H, d, rows, nrows, out, lse);
+}
+
+/*
+ * attention_row over double keys and values (the stage step's fresh rows are
+ * projections, not values of the I/O type).  Same definition as above.
+ */
+static void attention_row_d(const double* q, const double* k, const double* v, int64_t nk,
+                            int64_t row_stride, int64_t d, double scale, double* s, double* o) {
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    if (nk == 0) return;
+    double m = -INFINITY;
+    for (int64_t j = 0; j < nk; ++j) {
+        const double* kj = k + j * row_stride;
+        double dot = 0.0;
+        for (int64_t c = 0; c < d; ++c) dot += q[c] * kj[c];
+        s[j] = dot * scale;
+        if (s[j] > m) m = s[j];
+    }
+    double l = 0.0;
+    for (int64_t j = 0; j < nk; ++j) l += exp(s[j] - m);
+    const double lse_j = m + log(l);
+    for (int64_t j = 0; j < nk; ++j) {
+        const double p = exp(s[j] - lse_j);
+        const double* vj = v + j * row_stride;
+        for (int64_t c = 0; c < d; ++c) o[c] += p * vj[c];
+    }
+}
+
+/*
+ * One PipeFusion stage micro-step at one attention layer (Section 4.1.2: a
+ * device runs a patch through its layers; Section 3: the QKV projections
+ * come before self-attention, and the attention output is projected back):
+ *
+ *   q = x Wq,  k = x Wk,  v = x Wv      x [B, L, C], W [C, H*d]
+ *   patch step: rows [off, off+L) of the buffer take (k, v); the patch's
+ *               queries attend over the whole buffer (stale rows elsewhere)
+ *   y = o Wo                            o [B, L, H*d], Wo [H*d, C]
+ *
+ * No biases, norms or gates.  Products and sums in double; the fresh rows
+ * are stored into kv_buf rounded to float (kv_buf [2, B, N, H, d] in/out).
+ * rows/nrows select the patch rows whose outputs are evaluated (NULL = all
+ * L in order); y is [B, nrows, C] and o (may be NULL) [B, nrows, H, d],
+ * double; pq/pk/pv (each may be NULL) receive q/k/v [B, L, H, d], double.
+ */
+int xo_stage(const float* x, const float* wq, const float* wk, const float* wv, const float* wo,
+             float* kv_buf, int64_t off, int64_t L, int64_t B, int64_t N, int64_t H, int64_t d,
+             int64_t C, const int64_t* rows, int64_t nrows, double* y, double* o, double* pq,
+             double* pk, double* pv) {
+    if (B < 0 || L < 0 || N < 0 || H <= 0 || d <= 0 || C <= 0 || nrows < 0) return -1;
+    if (off < 0 || off + L > N) return -1;
+    if (rows == NULL && nrows != L) return -1;
+    for (int64_t r = 0; rows != NULL && r < nrows; ++r)
+        if (rows[r] < 0 || rows[r] >= L) return -1;
+    const int64_t HD = H * d, plane = B * N * HD;
+    double* q = (double*)malloc(sizeof(double) * (size_t)(B * L * HD + 1));
+    double* kd = (double*)malloc(sizeof(double) * (size_t)(B * N * HD + 1));
+    double* vd = (double*)malloc(sizeof(double) * (size_t)(B * N * HD + 1));
+    double* ob = (double*)malloc(sizeof(double) * (size_t)(B * nrows * HD + 1));
+    if (!q || !kd || !vd || !ob) {
+        free(q); free(kd); free(vd); free(ob);
+        return -2;
+    }
+    /* stale rows of the buffer, then the projections of the patch rows */
+    for (int64_t t = 0; t < plane; ++t) {
+        kd[t] = (double)kv_buf[t];
+        vd[t] = (double)kv_buf[plane + t];
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < B * L; ++t) {
+        const int64_t b = t / L, i = t % L;
+        const float* xr = x + t * C;
+        double* qr = q + t * HD;
+        double* kr = kd + (b * N + off + i) * HD;
+        double* vr = vd + (b * N + off + i) * HD;
+        for (int64_t n = 0; n < HD; ++n) {
+            double sq = 0.0, sk = 0.0, sv = 0.0;
+            for (int64_t c = 0; c < C; ++c) {
+                sq += (double)xr[c] * (double)wq[c * HD + n];
+                sk += (double)xr[c] * (double)wk[c * HD + n];
+                sv += (double)xr[c] * (double)wv[c * HD + n];
+            }
+            qr[n] = sq;
+            kr[n] = sk;
+            vr[n] = sv;
+        }
+    }
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t i = 0; i < L; ++i)
+            for (int64_t n = 0; n < HD; ++n) {
+                const int64_t at = (b * N + off + i) * HD + n;
+                kv_buf[at] = (float)kd[at];
+                kv_buf[plane + at] = (float)vd[at];
+                if (pq) pq[(b * L + i) * HD + n] = q[(b * L + i) * HD + n];
+                if (pk) pk[(b * L + i) * HD + n] = kd[at];
+                if (pv) pv[(b * L + i) * HD + n] = vd[at];
+            }
+    const double inv_sqrt_d = 1.0 / sqrt((double)d);
+    const int64_t total = B * H * nrows;
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1));
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t t = 0; t < total; ++t) {
+            const int64_t r = t % nrows;
+            const int64_t h = (t / nrows) % H;
+            const int64_t b = t / (nrows * H);
+            const int64_t i = rows ? rows[r] : r;
+            attention_row_d(q + (b * L + i) * HD + h * d, kd + b * N * HD + h * d,
+                            vd + b * N * HD + h * d, N, HD, d, inv_sqrt_d, s,
+                            ob + (b * nrows + r) * HD + h * d);
+        }
+        free(s);
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < B * nrows; ++t) {
+        const double* orow = ob + t * HD;
+        for (int64_t c = 0; c < C; ++c) {
+            double acc = 0.0;
+            for (int64_t n = 0; n < HD; ++n) acc += orow[n] * (double)wo[n * C + c];
+            y[t * C + c] = acc;
+        }
+        if (o)
+            for (int64_t n = 0; n < HD; ++n) o[t * HD + n] = orow[n];
+    }
+    free(q); free(kd); free(vd); free(ob);
+    return 0;
 }

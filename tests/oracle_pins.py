@@ -406,7 +406,81 @@ def pin_patch_ranges_sp_shards(orc):
     _close(np.concatenate(lses, axis=2), lb, TOL, "sharded queries lse")
 
 
+def _stage_inputs(B, L, N, H, d, C, seed):
+    x = random_io((B, L, C), "bf16", seed)
+    w = [random_io((C, H * d), "bf16", seed + s, 1.0 / math.sqrt(C)) for s in (1, 2, 3)]
+    wo = random_io((H * d, C), "bf16", seed + 4, 1.0 / math.sqrt(H * d))
+    kv = np.ascontiguousarray(random_io((2, B, N, H, d), "bf16", seed + 5))
+    return x, w, wo, kv
+
+
+def pin_stage_brute_force(orc):
+    """Stage micro-step on tiny inputs by its definition in pure Python: the
+    projections as math.fsum dot products, the patch step with the direct
+    softmax (no max shift), the output projection; also the buffer's fresh
+    rows (the projections rounded to float) and the returned q/k/v."""
+    B, L, N, H, d, C, off = 2, 3, 7, 2, 3, 5, 2
+    x, (wq, wk, wv), wo, kv = _stage_inputs(B, L, N, H, d, C, 70)
+    kv0 = kv.copy()
+    res = orc.stage_step(x, wq, wk, wv, wo, kv, off)
+
+    def proj(w):
+        out = np.zeros((B, L, H, d))
+        for b, i, h, c in itertools.product(range(B), range(L), range(H), range(d)):
+            out[b, i, h, c] = math.fsum(float(x[b, i, e]) * float(w[e, h * d + c]) for e in range(C))
+        return out
+    q, k, v = proj(wq), proj(wk), proj(wv)
+    kb, vb = kv0[0].astype(np.float64), kv0[1].astype(np.float64)
+    kb[:, off:off + L], vb[:, off:off + L] = k, v
+    o, _ = brute_attention(q, kb, vb)
+    y = np.zeros((B, L, C))
+    for b, i, e in itertools.product(range(B), range(L), range(C)):
+        y[b, i, e] = math.fsum(o[b, i, n // d, n % d] * float(wo[n, e]) for n in range(H * d))
+    _close(res["q"], q, TOL, "stage q")
+    _close(res["k"], k, TOL, "stage k")
+    _close(res["v"], v, TOL, "stage v")
+    _close(res["o"], o, TOL, "stage attention output")
+    _close(res["y"], y, TOL, "stage y")
+    exp_kv = kv0.copy()
+    exp_kv[0][:, off:off + L], exp_kv[1][:, off:off + L] = k.astype(np.float32), v.astype(np.float32)
+    assert np.array_equal(kv, exp_kv), "stage buffer update"
+
+
+def pin_stage_identity_is_patch_step(orc):
+    """With C = H*d and every projection the identity, the stage micro-step
+    is the patch step with q = k = v = x (the pinned patch oracle), and the
+    output projection returns its output unchanged."""
+    B, L, N, H, d, off = 2, 4, 9, 2, 3, 3
+    C = H * d
+    x = random_io((B, L, C), "bf16", 80)
+    kv = np.ascontiguousarray(random_io((2, B, N, H, d), "bf16", 81))
+    kv_p = kv.copy()
+    eye = np.eye(C, dtype=np.float32)
+    res = orc.stage_step(x, eye, eye, eye, eye, kv, off)
+    xq = x.reshape(B, L, H, d)
+    o, _ = orc.patch(xq, kv_p, off, xq, xq)
+    _close(res["o"], o, TOL, "identity stage vs patch step")
+    _close(res["y"], o.reshape(B, L, C), TOL, "identity output projection")
+    assert np.array_equal(kv, kv_p), "identity stage buffer vs patch step buffer"
+
+
+def pin_stage_head_permutation(orc):
+    """Multi-head attention does not depend on the order of its heads:
+    permuting the heads of Wq, Wk, Wv (columns), of Wo (rows) and of the
+    buffer leaves y unchanged, and permutes the attention output's heads."""
+    B, L, N, H, d, C, off = 1, 3, 8, 3, 2, 4, 4
+    x, (wq, wk, wv), wo, kv = _stage_inputs(B, L, N, H, d, C, 90)
+    perm = [2, 0, 1]
+    cols = np.concatenate([np.arange(h * d, (h + 1) * d) for h in perm])
+    res = orc.stage_step(x, wq, wk, wv, wo, kv.copy(), off)
+    kvp = np.ascontiguousarray(kv[:, :, :, perm, :])
+    resp = orc.stage_step(x, wq[:, cols], wk[:, cols], wv[:, cols], wo[cols, :], kvp, off)
+    _close(resp["y"], res["y"], 1e-12, "head-permuted stage y")
+    _close(resp["o"], res["o"][:, :, perm, :], 1e-12, "head-permuted stage o")
+
+
 PINS = [pin_brute_force, pin_scipy_softmax, pin_closed_forms, pin_empty_and_rows,
         pin_permutation_and_independence, pin_merge_equals_full, pin_merge_algebra,
         pin_patch_update_exact, pin_patch_semantics, pin_patch_ranges_brute_force,
-        pin_patch_ranges_in_context, pin_patch_ranges_sp_shards]
+        pin_patch_ranges_in_context, pin_patch_ranges_sp_shards, pin_stage_brute_force,
+        pin_stage_identity_is_patch_step, pin_stage_head_permutation]

@@ -55,6 +55,14 @@ MUTANTS = [
     ("ranged step attends over the fresh rows only",
      "return xo_attention(q, kv_buf, kv_buf + plane, B, Nq, N, H, d, rows, nrows, out, lse);",
      "return xo_attention(q, fresh_k, fresh_v, B, Nq, F, H, d, rows, nrows, out, lse);"),
+    ("stage keys projected with Wq", "sk += (double)xr[c] * (double)wk[c * HD + n];",
+     "sk += (double)xr[c] * (double)wq[c * HD + n];"),
+    ("stage attends over stale keys", "            kr[n] = sk;\n", "            (void)sk;\n"),
+    ("stage output projection uses Wo transposed", "acc += orow[n] * (double)wo[n * C + c];",
+     "acc += orow[n] * (double)wo[(c * HD + n) % (HD * C)];"),
+    ("stage skips the output projection rows past the first",
+     "for (int64_t t = 0; t < B * nrows; ++t) {\n        const double* orow",
+     "for (int64_t t = 0; t < (B * nrows > 0 ? 1 : 0); ++t) {\n        const double* orow"),
 ]
 
 
