@@ -68,6 +68,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="pixart",
                     choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "sd3_ic_bal", "pixart_hybrid",
+                             "pixart_stage",
                              "flux_ring"])
     ap.add_argument("--no-split", action="store_true",
                     help="never split a query tile's keys over several workgroups")
@@ -86,8 +87,18 @@ def cpu_baseline(w, t, target_s: float):
     import oracle
 
     orc = oracle.get()
-    jobs = []  # (description, nq_total, nk, run(rows))
-    if w.patches():
+    jobs = []  # (description, nq_total, nk, run(rows), flops(rows))
+    attn = lambda nq, nk: w.attn_flops(nq, nk)
+    if w.hidden:
+        kv = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
+        ws = [t.extra[n] for n in ("wq", "wk", "wv", "wo")]
+        C, HD = w.hidden, w.H * w.d
+        for p, (off, ln) in enumerate(w.patches()):
+            x = t.extra["x"][:, off:off + ln].copy()
+            jobs.append((f"stage micro-step {p}", ln, w.N,
+                         lambda rows, x=x, off=off: orc.stage_step(x, *ws, kv, off, rows=rows),
+                         lambda n, ln=ln: attn(n, w.N) + 2.0 * w.B * C * HD * (3 * ln + n)))
+    elif w.patches():
         kv = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
         for p, (ranges, qrows) in enumerate(w.patch_calls()):
             frows = np.concatenate([np.arange(o, o + n) for o, n in ranges])
@@ -96,7 +107,8 @@ def cpu_baseline(w, t, target_s: float):
             fv = t.v_fresh[:, frows].copy()
             jobs.append((f"patch step {p}", len(qrows), w.N,
                          lambda rows, q=q, ranges=ranges, fk=fk, fv=fv:
-                         orc.patch_ranges(q, kv, ranges, fk, fv, rows=rows)))
+                         orc.patch_ranges(q, kv, ranges, fk, fv, rows=rows),
+                         lambda n: attn(n, w.N)))
     else:
         q0, q1 = w.sp_q
         q = t.q[:, q0:q1].copy()
@@ -104,11 +116,12 @@ def cpu_baseline(w, t, target_s: float):
             k = t.k_fresh[:, s:e].copy()
             v = t.v_fresh[:, s:e].copy()
             jobs.append((f"chunk {r}", q1 - q0, e - s,
-                         lambda rows, k=k, v=v: orc.attention(q, k, v, rows=rows)))
+                         lambda rows, k=k, v=v: orc.attention(q, k, v, rows=rows),
+                         lambda n, nk=e - s: attn(n, nk)))
 
     # calibrate the cost of one (query row x key) on a few rows of the first
     # call; the first probe also starts the oracle's thread pool
-    desc0, nq0, nk0, run0 = jobs[0]
+    desc0, nq0, nk0, run0, _ = jobs[0]
     probe = np.linspace(0, nq0 - 1, min(64, nq0)).astype(np.int64)
     run0(probe)
     t0 = time.perf_counter()
@@ -118,7 +131,7 @@ def cpu_baseline(w, t, target_s: float):
     # call cut to an evenly spaced subset of its rows to stay near target_s
     flops, spent, parts = 0.0, 0.0, []
     for rep in range(1000):
-        for desc, nq, nk, run in jobs:
+        for desc, nq, nk, run, flops_of in jobs:
             left = target_s - spent
             if left <= 0.05 * target_s:
                 break
@@ -130,7 +143,7 @@ def cpu_baseline(w, t, target_s: float):
             dt = time.perf_counter() - t0
             spent += dt
             per_unit = dt / (len(rows) * nk)
-            flops += w.attn_flops(len(rows), nk)
+            flops += flops_of(len(rows))
             parts.append(f"{desc} ({len(rows)}/{nq} rows)")
         else:
             continue
@@ -172,8 +185,9 @@ def main():
 
     # each entry: (kind, callable, flops, bytes)
     calls = []
+    patch_kind = "stage_step" if hp.stage is not None else "patch_attn"
     for p in range(len(hp.patch_q)):
-        calls.append(("patch_attn", lambda p=p: hp.patch_step(p), hp.patch_flops(p), 0.0))
+        calls.append((patch_kind, lambda p=p: hp.patch_step(p), hp.patch_flops(p), 0.0))
     if hp.sp_q is not None:
         for r in range(len(hp.chunk_k)):
             calls.append(("chunk_attn", lambda r=r: hp.chunk_step(r), hp.chunk_flops(r), 0.0))
@@ -314,7 +328,9 @@ def main():
     if dd["flops"]:
         per_launch = dd["flops"] / dd["launches"]
         achieved = per_launch / avg_s / 1e12
-        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+        # bf16 attention runs on the matrix cores; the f32 path is plain VALU code
+        roof = {"kernel": dom, "bound": "mfma" if w.dtype == "bf16" else "alu",
+                "achieved": round(achieved, 2), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
     else:
         per_launch = dd["bytes"] / dd["launches"]
@@ -342,6 +358,9 @@ def main():
                           " 220 image + 333 text)",
             "flux_ring": "flux-2048px SP share, ring form: B=1 H=24 d=128, Q 4224 rows, 4 chunks"
                          " of 4224 each merged into the running output as it arrives",
+            "pixart_stage": "pixart-1024px stage micro-steps: B=2 H=16 d=72 hidden 1152, 4096"
+                            " tokens, M=4 x (QKV projections, patch step, output projection);"
+                            " value counts projection and attention FLOPs",
             "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"
                              " 4096 tokens, M=4 patch steps of 1024 gathered fresh rows,"
                              " 512 local queries each"}[w.name]

@@ -224,6 +224,40 @@ int xdit_kv_update(void* kv_buf, int64_t patch_off, int64_t patch_len, const voi
                    const void* fresh_v, int64_t batch, int64_t seq_len, int64_t heads,
                    int64_t head_dim, int32_t dtype);
 
+/*
+ * One PipeFusion stage micro-step at one attention layer (Section 4.1.2: a
+ * device runs each patch through its stage's layers; Section 3: QKV
+ * projections come before self-attention, whose output is projected back):
+ *
+ *   q = x wq,  k = x wk,  v = x wv      (projections of the patch's rows)
+ *   the patch step of xdit_patch_attn with fresh K/V = (k, v), output o
+ *   y = o wo
+ *
+ *   x          [B, patch_len, C]        the patch's hidden states, C = hidden
+ *   wq, wk, wv [C, H*d]                 row-major, so q[b, i] = x[b, i] wq
+ *   wo         [H*d, C]
+ *   kv_buf     [2, B, seq_len, H, d]    MUTATED as by xdit_patch_attn: rows
+ *                                       [patch_off, patch_off + patch_len)
+ *                                       take k and v bit for bit
+ *   q, k, v, o [B, patch_len, H, d]     caller-owned intermediates, written
+ *   y          [B, patch_len, C]        output
+ * bf16 only (XDIT_ERR_UNSUPPORTED otherwise); the GEMMs (hipBLASLt) and the
+ * attention accumulate in float32 and round each result to bf16.  No
+ * biases, norms or gates.  No output may overlap another buffer or any
+ * input; other requirements as for xdit_patch_attn; 1 <= hidden <= 65536.
+ * The library allocates nothing itself; hipBLASLt keeps one handle per
+ * device and per-shape plans from the first call on (its own host and
+ * device memory).  The first call of each shape times hipBLASLt's candidate
+ * algorithms on its own operands and synchronises the calling stream (so it
+ * must not run under graph capture); later calls only launch.
+ * XDIT_ERR_HIP if hipBLASLt refuses a GEMM.  Five launches on the calling
+ * thread's stream.
+ */
+int xdit_stage_step(const void* x, const void* wq, const void* wk, const void* wv, const void* wo,
+                    void* kv_buf, int64_t patch_off, int64_t patch_len, void* q, void* k, void* v,
+                    void* o, void* y, int64_t batch, int64_t seq_len, int64_t heads,
+                    int64_t head_dim, int64_t hidden, int32_t dtype);
+
 /* Stream for the calling thread's later launches (a hipStream_t; NULL = the
  * default stream).  Always returns XDIT_OK. */
 int xdit_set_stream(void* stream);

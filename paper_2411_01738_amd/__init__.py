@@ -19,7 +19,7 @@ from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XDIT
 __all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
            "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
            "split_workspace_bytes", "xdit_lse_merge",
-           "xdit_kv_update", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
+           "xdit_kv_update", "xdit_stage_step", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
            "version"]
 
 
@@ -240,3 +240,31 @@ def xdit_kv_update(kv_buf, patch_off: int, patch_len: int, fresh_k, fresh_v) -> 
     _use_current_stream()
     check(lib().xdit_kv_update(_ptr(kv_buf), int(patch_off), int(patch_len), _ptr(fresh_k),
                                _ptr(fresh_v), B, N, H, d, _dtype_code(kv_buf)))
+
+
+def xdit_stage_step(x, wq, wk, wv, wo, kv_buf, patch_off: int, q, k, v, o, y) -> None:
+    """One PipeFusion stage micro-step at one attention layer: q/k/v = x
+    W{q,k,v} (x [B,L,C], W [C,H*d]), the patch step over kv_buf [2,B,N,H,d]
+    at rows [patch_off, patch_off+L) with fresh K/V (k, v) and output o, then
+    y = o wo (wo [H*d,C]).  q, k, v, o [B,L,H,d] and y [B,L,C] are written."""
+    _dense(kv_buf, "kv_buf", 5)
+    _, B, N, H, d = kv_buf.shape
+    _dense(x, "x", 3)
+    L, C = x.shape[1], x.shape[2]
+    if x.shape[0] != B:
+        raise XditError(-3, f"x must be [B, L, C] with B = {B}")
+    for t, nm, shp in ((wq, "wq", (C, H * d)), (wk, "wk", (C, H * d)), (wv, "wv", (C, H * d)),
+                       (wo, "wo", (H * d, C)), (y, "y", (B, L, C))):
+        _dense(t, nm, len(shp))
+        if tuple(t.shape) != shp or t.dtype != x.dtype:
+            raise XditError(-3, f"{nm} must be {shp} of x's dtype")
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _dense(t, nm, 4)
+        if tuple(t.shape) != (B, L, H, d) or t.dtype != x.dtype:
+            raise XditError(-3, f"{nm} must be {(B, L, H, d)} of x's dtype")
+    if kv_buf.dtype != x.dtype:
+        raise XditError(-3, "kv_buf must have x's dtype")
+    _use_current_stream()
+    check(lib().xdit_stage_step(_ptr(x), _ptr(wq), _ptr(wk), _ptr(wv), _ptr(wo), _ptr(kv_buf),
+                                int(patch_off), L, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(y), B,
+                                N, H, d, C, _dtype_code(x)))

@@ -43,6 +43,8 @@ SIGNATURES = {
                                              _i32]),
     "xdit_lse_merge": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_kv_update": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
+    "xdit_stage_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp,
+                                       _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
     "xdit_set_stream": (ctypes.c_int, [_vp]),
     "xdit_get_stream": (_vp, []),
     "xdit_last_error": (ctypes.c_char_p, []),

@@ -5,10 +5,15 @@
 #include "../../include/xdit.h"
 
 #include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
 
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "kernels.h"
 
@@ -521,3 +526,144 @@ int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n,
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The stage micro-step's projections: plain bf16 GEMMs with float32
+// accumulation through hipBLASLt, one handle per device and one plan per
+// shape, both created on first use and kept for the life of the process.  A
+// plan holds the layouts and the fastest of hipBLASLt's candidate
+// algorithms that need no workspace, timed on the first call's own operands
+// (a few runs each on the calling stream, which that first call therefore
+// synchronises).
+namespace {
+
+struct GemmPlan {
+    hipblasLtMatmulDesc_t desc = nullptr;
+    hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, ld = nullptr;
+    hipblasLtMatmulAlgo_t algo{};
+};
+
+std::mutex g_gemm_mutex;
+std::map<int, hipblasLtHandle_t> g_handles;
+std::map<std::tuple<int, int64_t, int64_t, int64_t>, GemmPlan> g_plans;
+
+int blas_status(hipblasStatus_t st, const char* what) {
+    if (st != HIPBLAS_STATUS_SUCCESS) return fail(XDIT_ERR_HIP, "%s: hipBLASLt status %d", what, (int)st);
+    return XDIT_OK;
+}
+
+// Row-major C[M, N] = A[M, K] B[K, N], all bf16 and contiguous.  In
+// hipBLASLt's column-major terms that is C^T (N x M) = B^T (N x K) A^T (K x M),
+// where B^T and A^T are the row-major buffers read as column-major.
+int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K) {
+    if (M == 0 || N == 0) return XDIT_OK;
+    int dev = 0;
+    XDIT_TRY(hip_status(hipGetDevice(&dev), fn));
+    std::lock_guard<std::mutex> lock(g_gemm_mutex);
+    auto hit = g_handles.find(dev);
+    if (hit == g_handles.end()) {
+        hipblasLtHandle_t h = nullptr;
+        XDIT_TRY(blas_status(hipblasLtCreate(&h), "hipblasLtCreate"));
+        hit = g_handles.emplace(dev, h).first;
+    }
+    const hipblasLtHandle_t handle = hit->second;
+    const auto key = std::make_tuple(dev, M, N, K);
+    auto pit = g_plans.find(key);
+    if (pit == g_plans.end()) {
+        GemmPlan pl;
+        XDIT_TRY(blas_status(hipblasLtMatmulDescCreate(&pl.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F),
+                             "hipblasLtMatmulDescCreate"));
+        const hipblasOperation_t op = HIPBLAS_OP_N;
+        XDIT_TRY(blas_status(hipblasLtMatmulDescSetAttribute(pl.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &op, sizeof(op)),
+                             "hipblasLtMatmulDescSetAttribute"));
+        XDIT_TRY(blas_status(hipblasLtMatmulDescSetAttribute(pl.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &op, sizeof(op)),
+                             "hipblasLtMatmulDescSetAttribute"));
+        XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.la, HIP_R_16BF, N, K, N), "hipblasLtMatrixLayoutCreate"));
+        XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.lb, HIP_R_16BF, K, M, K), "hipblasLtMatrixLayoutCreate"));
+        XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.ld, HIP_R_16BF, N, M, N), "hipblasLtMatrixLayoutCreate"));
+        hipblasLtMatmulPreference_t pref = nullptr;
+        XDIT_TRY(blas_status(hipblasLtMatmulPreferenceCreate(&pref), "hipblasLtMatmulPreferenceCreate"));
+        uint64_t ws = 0;
+        hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &ws, sizeof(ws));
+        constexpr int kCands = 16;
+        hipblasLtMatmulHeuristicResult_t res[kCands];
+        int nres = 0;
+        const hipblasStatus_t st = hipblasLtMatmulAlgoGetHeuristic(handle, pl.desc, pl.la, pl.lb, pl.ld, pl.ld, pref,
+                                                                   kCands, res, &nres);
+        hipblasLtMatmulPreferenceDestroy(pref);
+        XDIT_TRY(blas_status(st, "hipblasLtMatmulAlgoGetHeuristic"));
+        if (nres < 1)
+            return fail(XDIT_ERR_HIP, "%s: hipBLASLt has no algorithm for a %lld x %lld x %lld bf16 GEMM", fn,
+                        (long long)M, (long long)N, (long long)K);
+        pl.algo = res[0].algo;
+        if (nres > 1) {
+            hipEvent_t e0 = nullptr, e1 = nullptr;
+            XDIT_TRY(hip_status(hipEventCreate(&e0), fn));
+            XDIT_TRY(hip_status(hipEventCreate(&e1), fn));
+            const float one = 1.f, zero = 0.f;
+            float best = 1e30f;
+            for (int i = 0; i < nres; ++i) {
+                if (res[i].state != HIPBLAS_STATUS_SUCCESS || res[i].workspaceSize != 0) continue;
+                bool ok = true;
+                for (int r = 0; r < 8 && ok; ++r) {
+                    if (r == 2) ok = hipEventRecord(e0, g_stream) == hipSuccess;
+                    ok = ok && hipblasLtMatmul(handle, pl.desc, &one, B, pl.la, A, pl.lb, &zero, C, pl.ld, C, pl.ld,
+                                               &res[i].algo, nullptr, 0, g_stream) == HIPBLAS_STATUS_SUCCESS;
+                }
+                float ms = 0.f;
+                ok = ok && hipEventRecord(e1, g_stream) == hipSuccess && hipEventSynchronize(e1) == hipSuccess &&
+                     hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+                if (ok && ms < best) {
+                    best = ms;
+                    pl.algo = res[i].algo;
+                }
+            }
+            hipEventDestroy(e0);
+            hipEventDestroy(e1);
+        }
+        pit = g_plans.emplace(key, pl).first;
+    }
+    const GemmPlan& pl = pit->second;
+    const float alpha = 1.f, beta = 0.f;
+    return blas_status(hipblasLtMatmul(handle, pl.desc, &alpha, B, pl.la, A, pl.lb, &beta, C, pl.ld, C, pl.ld,
+                                       &pl.algo, nullptr, 0, g_stream),
+                       fn);
+}
+
+}  // namespace
+
+extern "C" int xdit_stage_step(const void* x, const void* wq, const void* wk, const void* wv,
+                               const void* wo, void* kv_buf, int64_t patch_off, int64_t patch_len,
+                               void* q, void* k, void* v, void* o, void* y, int64_t batch,
+                               int64_t seq_len, int64_t heads, int64_t head_dim, int64_t hidden,
+                               int32_t dtype) {
+    clear_error();
+    const char* fn = "xdit_stage_step";
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    if (dtype != XDIT_BF16) return fail(XDIT_ERR_UNSUPPORTED, "%s: bf16 only", fn);
+    if (hidden <= 0 || hidden > 65536) return fail(XDIT_ERR_SHAPE, "%s: hidden = %lld outside [1, 65536]", fn,
+                                                   (long long)hidden);
+    XDIT_TRY(check_patch_args(fn, q, kv_buf, patch_off, patch_len, k, v, o, batch, seq_len, heads, head_dim,
+                              dtype));
+    const int64_t HD = heads * head_dim, M = batch * patch_len;
+    const Span sx{x, M * hidden * 2, "x"}, sy{y, M * hidden * 2, "y"}, swq{wq, hidden * HD * 2, "wq"},
+        swk{wk, hidden * HD * 2, "wk"}, swv{wv, hidden * HD * 2, "wv"}, swo{wo, HD * hidden * 2, "wo"},
+        sb{kv_buf, 2 * batch * seq_len * HD * 2, "kv_buf"}, sq{q, M * HD * 2, "q"}, sk{k, M * HD * 2, "k"},
+        sv{v, M * HD * 2, "v"}, so{o, M * HD * 2, "o"};
+    const Span* ins[] = {&sx, &swq, &swk, &swv, &swo};
+    const Span* outs[] = {&sq, &sk, &sv, &so, &sy};
+    for (const Span* s : ins) XDIT_TRY(check_ptr(*s));
+    for (const Span* s : outs) XDIT_TRY(check_ptr(*s));
+    for (int i = 0; i < 5; ++i) {
+        XDIT_TRY(check_no_overlap(*outs[i], sb));
+        for (const Span* s : ins) XDIT_TRY(check_no_overlap(*outs[i], *s));
+        for (int j = 0; j < i; ++j) XDIT_TRY(check_no_overlap(*outs[i], *outs[j]));
+    }
+    if (M == 0 || heads == 0) return XDIT_OK;
+    XDIT_TRY(gemm_bf16(fn, x, wq, q, M, HD, hidden));
+    XDIT_TRY(gemm_bf16(fn, x, wk, k, M, HD, hidden));
+    XDIT_TRY(gemm_bf16(fn, x, wv, v, M, HD, hidden));
+    XDIT_TRY(patch_ranges_impl(fn, q, patch_len, kv_buf, 1, &patch_off, &patch_len, k, v, o, nullptr, batch,
+                               seq_len, heads, head_dim, dtype));
+    return gemm_bf16(fn, o, wo, y, M, hidden, HD);
+}

@@ -6,6 +6,9 @@ A step is one pass over every part of the path for one layer:
     with in-context conditioning, and attends over the buffer with the
     patch's queries, or this GPU's shard of them under hybrid parallelism;
     Sections 4.1.2 and 4.1.4), and
+    With a hidden size, each patch step is a stage micro-step instead: the
+    patch rows' QKV projections, the patch step, the output projection
+    (Section 4.1.2).
   * the sequence-parallel share: chunk attention of the local query shard
     against each K/V chunk, then the log-sum-exp merge of the partials
     (Section 4.1.1).
@@ -20,7 +23,7 @@ import numpy as np
 
 from . import (split_workspace_bytes, xdit_chunk_attn, xdit_chunk_attn_accum,
                xdit_chunk_attn_split, xdit_lse_merge, xdit_patch_attn, xdit_patch_attn_ranges,
-               xdit_patch_attn_split)
+               xdit_patch_attn_split, xdit_stage_step)
 from .inputs import Tensors, Workload
 
 
@@ -51,6 +54,19 @@ class HotPath:
             self.patch_k.append(up(t.k_fresh[:, frows]))
             self.patch_v.append(up(t.v_fresh[:, frows]))
             self.patch_out.append(torch.empty((B, len(qrows), H, d), device=device, dtype=dt))
+        # stage micro-steps: hidden states of the patch rows, the projections,
+        # and the intermediates the library writes
+        self.stage = None
+        if w.hidden:
+            C = w.hidden
+            self.stage = {"w": [up(t.extra[n]) for n in ("wq", "wk", "wv", "wo")],
+                          "x": [], "y": [], "qkvo": []}
+            for ranges, qrows in self.calls:
+                (off, ln), = ranges
+                self.stage["x"].append(up(t.extra["x"][:, off:off + ln]))
+                self.stage["y"].append(torch.empty((B, ln, C), device=device, dtype=dt))
+                self.stage["qkvo"].append([torch.empty((B, ln, H, d), device=device, dtype=dt)
+                                           for _ in range(4)])
         self.sp_q = self.sp_out = self.sp_lse = None
         self.chunk_k, self.chunk_v, self.chunk_out, self.chunk_lse = [], [], [], []
         if w.sp_chunks:
@@ -70,7 +86,7 @@ class HotPath:
         need = 0
         self.patch_split = [False] * len(self.calls)
         self.chunk_split = False
-        if split:
+        if split and self.stage is None:
             for p in range(len(self.calls)):
                 n = split_workspace_bytes(self.patch_q[p], w.N)
                 self.patch_split[p] = n > 0
@@ -88,7 +104,11 @@ class HotPath:
 
     def patch_step(self, p: int) -> None:
         ranges, qrows = self.calls[p]
-        if self.patch_split[p]:
+        if self.stage is not None:
+            st = self.stage
+            xdit_stage_step(st["x"][p], *st["w"], self.kv_buf, ranges[0][0], *st["qkvo"][p],
+                            st["y"][p])
+        elif self.patch_split[p]:
             xdit_patch_attn_split(self.patch_q[p], self.kv_buf, ranges, self.patch_k[p],
                                   self.patch_v[p], self.patch_out[p], None, 0, self.workspace)
         elif len(ranges) == 1 and len(qrows) == ranges[0][1]:
@@ -129,7 +149,15 @@ class HotPath:
 
     # -- accounting ----------------------------------------------------------
     def patch_flops(self, p: int) -> float:
-        return self.w.attn_flops(len(self.calls[p][1]), self.w.N)
+        f = self.w.attn_flops(len(self.calls[p][1]), self.w.N)
+        if self.stage is not None:
+            f += self.gemm_flops(p)
+        return f
+
+    def gemm_flops(self, p: int) -> float:
+        """The stage micro-step's four projections, 2*B*L*C*(H*d) each."""
+        w = self.w
+        return 4 * 2.0 * w.B * len(self.calls[p][1]) * w.hidden * w.H * w.d if w.hidden else 0.0
 
     def chunk_flops(self, r: int) -> float:
         s, e = self.w.sp_chunks[r]

@@ -42,6 +42,8 @@ class Workload:
                               # first 1/sp_degree of each patch step's query rows
     sp_ring: bool = False     # SP chunks merged into a running (out, lse) one by one
                               # instead of stored as partials and merged at the end
+    hidden: int = 0           # > 0: each patch step is a stage micro-step with QKV
+                              # and output projections of this hidden size
     note: str = ""
 
     @property
@@ -122,6 +124,9 @@ WORKLOADS = {
                            balanced=True,
                            note="SD3 with in-context conditioning and a load-balanced image"
                                 " partition: patch 0 takes 220 image rows + the 333 text rows"),
+    "pixart_stage": Workload("pixart_stage", "bf16", 2, 16, 72, 4096, 0, 4, 1, hidden=1152,
+                             note="Pixart 1024px stage micro-steps: per patch, QKV projections"
+                                  " (hidden 1152), the patch step, the output projection"),
     "pixart_hybrid": Workload("pixart_hybrid", "bf16", 2, 16, 72, 4096, 0, 4, 1, sp_degree=2,
                               note="Pixart 1024px, PipeFusion x 2-way sequence parallelism:"
                                    " gathered fresh K/V, this GPU's half of each patch's"
@@ -169,7 +174,10 @@ def generate(w: Workload, seed: int | None = None) -> Tensors:
     """Draw, in this order from numpy PCG64(seed): Q, K, V [B, N, H, d], then
     the K and V staleness noise [B, n_img, H, d]; all standard normal float32.
     stale = fresh + 0.05 * noise on image rows (float32), then every tensor is
-    rounded to the I/O dtype."""
+    rounded to the I/O dtype.  With hidden = C > 0, the same generator then
+    draws the image rows' hidden states x [B, n_img, C] (standard normal) and
+    the projections wq, wk, wv [C, H*d] (scale 1/sqrt(C)) and wo [H*d, C]
+    (scale 1/sqrt(H*d)), kept in extra."""
     rng = np.random.Generator(np.random.PCG64(w.seed if seed is None else seed))
     shape = (w.B, w.N, w.H, w.d)
     q = rng.standard_normal(shape, dtype=np.float32)
@@ -180,8 +188,17 @@ def generate(w: Workload, seed: int | None = None) -> Tensors:
     k_stale[:, :w.n_img] += np.float32(0.05) * rng.standard_normal(nshape, dtype=np.float32)
     v_stale = v.copy()
     v_stale[:, :w.n_img] += np.float32(0.05) * rng.standard_normal(nshape, dtype=np.float32)
-    return Tensors(to_io(q, w.dtype), to_io(k, w.dtype), to_io(v, w.dtype),
-                   to_io(k_stale, w.dtype), to_io(v_stale, w.dtype))
+    t = Tensors(to_io(q, w.dtype), to_io(k, w.dtype), to_io(v, w.dtype),
+                to_io(k_stale, w.dtype), to_io(v_stale, w.dtype))
+    if w.hidden:
+        C, HD = w.hidden, w.H * w.d
+        t.extra["x"] = to_io(rng.standard_normal((w.B, w.n_img, C), dtype=np.float32), w.dtype)
+        for name in ("wq", "wk", "wv"):
+            t.extra[name] = to_io(rng.standard_normal((C, HD), dtype=np.float32)
+                                  * np.float32(1.0 / np.sqrt(C)), w.dtype)
+        t.extra["wo"] = to_io(rng.standard_normal((HD, C), dtype=np.float32)
+                              * np.float32(1.0 / np.sqrt(HD)), w.dtype)
+    return t
 
 
 def random_io(shape, dtype: str, seed: int, scale: float = 1.0) -> np.ndarray:

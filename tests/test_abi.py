@@ -29,7 +29,8 @@ def test_header_declares_the_entry_points():
     names = header_functions()
     for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
                "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
-               "xdit_split_workspace_bytes", "xdit_lse_merge", "xdit_kv_update", "xdit_set_stream",
+               "xdit_split_workspace_bytes", "xdit_lse_merge", "xdit_kv_update", "xdit_stage_step",
+               "xdit_set_stream",
                "xdit_get_stream", "xdit_last_error", "xdit_version"]:
         assert fn in names
 
@@ -204,6 +205,32 @@ def test_empty_calls_succeed_without_launching():
     assert lib.xdit_patch_attn_ranges(P(0), 8, P(1), 1, offs, lens, None, None, P(4), None,
                                       0, 16, 2, 64, 0) == 0
     assert lib.xdit_last_error().decode() == ""
+
+
+@needs_no_gpu
+def test_stage_rejections():
+    """Stage micro-step: bf16 only, hidden in range, slice inside the buffer,
+    aligned pointers, outputs overlapping nothing."""
+    lib = _lib.lib()
+    # x, wq, wk, wv, wo, kv_buf, off, len, q, k, v, o, y, B, N, H, d, C, dtype
+    ok = [P(0), P(1), P(2), P(3), P(4), P(5), 0, 8, P(6), P(7), P(8), P(9), P(10), 1, 16, 2, 64, 128, 0]
+
+    def call(**kw):
+        a = list(ok)
+        names = ["x", "wq", "wk", "wv", "wo", "kv", "off", "len", "q", "k", "v", "o", "y", "B", "N",
+                 "H", "d", "C", "dtype"]
+        for n, val in kw.items():
+            a[names.index(n)] = val
+        return lib.xdit_stage_step(*a)
+    assert call(dtype=1) == -7
+    assert call(C=0) == -3
+    assert call(off=12) == -4
+    assert call(q=None) == -1
+    assert call(x=P(0) + 8) == -5
+    assert call(y=P(0)) == -6
+    assert call(o=P(5)) == -6
+    assert call(k=P(6)) == -6
+    assert call(B=0, x=None, y=None, q=None, k=None, v=None, o=None) == 0
 
 
 def test_product_never_touches_the_oracle():

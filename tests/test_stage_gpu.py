@@ -1,0 +1,112 @@
+"""GPU parity of the PipeFusion stage micro-step (xdit_stage_step): QKV
+projections of the patch rows, the patch step, the output projection,
+against the fp64 oracle's stage step on the same seeded inputs.
+
+Tolerances (bf16): the projections are float32 GEMMs rounded to bf16, so
+q/k/v sit within half a bf16 ulp (2^-8 relative) of the exact products, plus
+float32 accumulation error.  The attention output and y inherit the
+attention kernel's bounds, widened by half for the effect of the rounded
+projections on the scores and of the rounded attention output on y."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2411_01738_amd import xdit_stage_step
+from paper_2411_01738_amd.hotpath import HotPath
+from paper_2411_01738_amd.inputs import WORKLOADS, generate, random_io, sample_rows
+from tests.gpu_util import to_gpu, to_np, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+STAGE_TOL = {"max_abs": 3e-2, "rms": 3e-3}
+
+
+def _close_rel(gpu, ref, what):
+    gpu, ref = np.asarray(gpu, np.float64), np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape, f"{what}: shape {gpu.shape} vs {ref.shape}"
+    bound = 2.0 ** -8 * np.abs(ref) + 1e-4
+    bad = np.abs(gpu - ref) > bound
+    assert not bad.any(), f"{what}: {bad.sum()} elements beyond half a bf16 ulp"
+
+
+def _close_out(gpu, ref, what):
+    gpu, ref = np.asarray(gpu, np.float64), np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape and np.all(np.isfinite(gpu)), what
+    err = np.abs(gpu - ref)
+    rms = float(np.sqrt(np.mean(err ** 2)))
+    assert err.max() <= STAGE_TOL["max_abs"], f"{what}: max abs err {err.max():.3e}"
+    assert rms <= STAGE_TOL["rms"], f"{what}: rms err {rms:.3e}"
+
+
+def _inputs(B, L, N, H, d, C, seed):
+    x = random_io((B, L, C), "bf16", seed)
+    ws = [random_io((C, H * d), "bf16", seed + s, 1.0 / math.sqrt(C)) for s in (1, 2, 3)]
+    wo = random_io((H * d, C), "bf16", seed + 4, 1.0 / math.sqrt(H * d))
+    kv = np.ascontiguousarray(random_io((2, B, N, H, d), "bf16", seed + 5))
+    return x, ws, wo, kv
+
+
+# (B, L, N, H, d, C, off): ragged lengths, hidden != H*d, a patch at the
+# buffer's start and at its end, a single-row patch, each head dimension
+CASES = [(2, 96, 320, 2, 72, 160, 64), (1, 130, 300, 3, 64, 192, 170),
+         (2, 64, 256, 2, 128, 256, 0), (1, 1, 128, 2, 64, 64, 127), (1, 200, 200, 1, 72, 72, 0)]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_L{}_N{}_H{}_d{}_C{}_off{}".format(*c))
+def test_stage_step(case):
+    torch = torch_mod()
+    B, L, N, H, d, C, off = case
+    x, (wq, wk, wv), wo, kv = _inputs(B, L, N, H, d, C, 700 + L)
+    print(f"[stage] {case}", flush=True)
+    g = {n: to_gpu(a, "bf16") for n, a in (("x", x), ("wq", wq), ("wk", wk), ("wv", wv), ("wo", wo),
+                                           ("kv", kv))}
+    q, k, v, o = (torch.empty((B, L, H, d), device="cuda", dtype=torch.bfloat16) for _ in range(4))
+    y = torch.empty((B, L, C), device="cuda", dtype=torch.bfloat16)
+    xdit_stage_step(g["x"], g["wq"], g["wk"], g["wv"], g["wo"], g["kv"], off, q, k, v, o, y)
+    torch.cuda.synchronize()
+    ref = oracle.get().stage_step(x, wq, wk, wv, wo, kv.copy(), off)
+    _close_rel(to_np(q), ref["q"], "q")
+    _close_rel(to_np(k), ref["k"], "k")
+    _close_rel(to_np(v), ref["v"], "v")
+    _close_out(to_np(o), ref["o"], "attention output")
+    _close_out(to_np(y), ref["y"], "y")
+    buf = to_np(g["kv"])
+    # the buffer's slice holds exactly the k/v the step produced; every
+    # other row is untouched
+    assert np.array_equal(buf[0][:, off:off + L], to_np(k)), "buffer K slice != k"
+    assert np.array_equal(buf[1][:, off:off + L], to_np(v)), "buffer V slice != v"
+    keep = np.ones(N, bool)
+    keep[off:off + L] = False
+    assert np.array_equal(buf[:, :, keep], kv[:, :, keep]), "rows outside the slice changed"
+
+
+def test_stage_steps_full_size_pixart():
+    """The four stage micro-steps of the Pixart workload in order (hidden
+    1152, 16 heads of 72), in the launch configuration the benchmark times;
+    sampled rows of each patch's y and attention output against the oracle,
+    the projections in full."""
+    torch = torch_mod()
+    orc = oracle.get()
+    w = WORKLOADS["pixart_stage"]
+    t = generate(w)
+    hp = HotPath(w, t)
+    kv_ref = np.ascontiguousarray(np.stack([t.k_stale, t.v_stale]))
+    ws = [t.extra[n] for n in ("wq", "wk", "wv", "wo")]
+    for p, (off, ln) in enumerate(w.patches()):
+        print(f"[pixart_stage] patch {p}", flush=True)
+        hp.patch_step(p)
+        torch.cuda.synchronize()
+        rows = sample_rows(ln, 29, [127, 128, ln - 1])
+        ref = orc.stage_step(t.extra["x"][:, off:off + ln], *ws, kv_ref, off, rows=rows)
+        q, k, v, o = (to_np(a) for a in hp.stage["qkvo"][p])
+        _close_rel(q, ref["q"], f"patch {p} q")
+        _close_rel(k, ref["k"], f"patch {p} k")
+        _close_rel(v, ref["v"], f"patch {p} v")
+        _close_out(o[:, rows], ref["o"], f"patch {p} attention output")
+        _close_out(to_np(hp.stage["y"][p])[:, rows], ref["y"], f"patch {p} y")
+        buf = to_np(hp.kv_buf)
+        assert np.array_equal(buf[0][:, off:off + ln], k) and np.array_equal(buf[1][:, off:off + ln], v)
