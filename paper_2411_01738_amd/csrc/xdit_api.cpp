@@ -618,8 +618,8 @@ int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, 
                     pl.algo = res[i].algo;
                 }
             }
-            hipEventDestroy(e0);
-            hipEventDestroy(e1);
+            (void)hipEventDestroy(e0);
+            (void)hipEventDestroy(e1);
         }
         pit = g_plans.emplace(key, pl).first;
     }
