@@ -60,6 +60,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -80,9 +81,13 @@ struct Cfg {
     static constexpr int BM = 32 * QB;               // query rows per workgroup
     static constexpr int BN = KS * KW;               // keys per tile
     static constexpr int DK = (D + 15) / 16 * 16;    // QK^T contraction length, padded to 16
-    static constexpr int DV = (D + 31) / 32 * 32;    // PV output rows, padded to 32
+    // PV output rows: DBLK full 32-row blocks; the rest (d = 72: dims 64..71)
+    // goes to one 16-row tail block, rows TB..TB+15, on the 16x16x32
+    // instruction
+    static constexpr int DBLK = D / 32;
+    static constexpr bool TAIL = D % 32 != 0;
+    static constexpr int TB = 32 * DBLK;             // first dim of the tail block
     static constexpr int KSTEPS = DK / 16;
-    static constexpr int DBLK = DV / 32;
     static constexpr int CH = D / 8;                 // 16-byte chunks per K/V row
     static constexpr int ROWB = 16 * CH;             // bytes per row in LDS
     // LDS layout of a row: logical chunk c sits in slot c ^ swz(row).  Both
@@ -120,14 +125,14 @@ struct Cfg {
     static constexpr int Q_PER_WAVE = (Q_PIECES + NW - 1) / NW;
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
-    static constexpr bool SUM_BY_MFMA = DV > D;      // a padding row of V^T holds ones
+    static constexpr bool SUM_BY_MFMA = TAIL;        // a padding row of V^T holds ones
     // end-of-sweep exchange: one slot (m, l, O^T accumulators) per query
     // block of each partial wave
-    static constexpr int XSLOT = 64 * (2 + 16 * DBLK);  // floats
+    static constexpr int XSLOT = 64 * (2 + 16 * DBLK + (TAIL ? 8 : 0));  // floats
     static constexpr int X_BYTES = 4 * QB * (KS - 1) * XSLOT;
     static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES > X_BYTES ? NSTAGE * STAGE_BYTES : X_BYTES;
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
-    static_assert(DV - D == 0 || DV - D == 24, "V padding handled for d = 72 only");
+    static_assert(!TAIL || (D - TB <= 15 && D - TB > 0 && KW % 32 == 0), "tail block: dims TB..D-1, then the ones row");
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
     static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads");
     static_assert(DMA_PER_TILE >= NW, "every wave loads part of each tile");
@@ -211,6 +216,12 @@ __device__ __forceinline__ void lds_wait_all(u32x2 (&r)[NS][NB][2]) {
     for (int i = 0; i < NS; ++i)
 #pragma unroll
         for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(r[i][j][0]), "+v"(r[i][j][1]));
+}
+// Registers filled by LDS reads that an earlier lds_wait_all has covered.
+template <int NT>
+__device__ __forceinline__ void lds_hold(u32x2 (&r)[NT][2]) {
+#pragma unroll
+    for (int i = 0; i < NT; ++i) asm volatile("" : "+v"(r[i][0]), "+v"(r[i][1]));
 }
 
 // Key of S^T row x (0..31) of a 32-key block: x = 16a + 8e + 4h + j is key
@@ -401,8 +412,13 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     //  d0+4q..+3 of key kw0 + 16ks + krow(8e + 4hf + j), where d0 = 32db +
     //  16*(group & 1) and e = 0, 1 selects the half k-step; lane i of the
     //  group then holds dim d0 + i of the four keys, in the order of the
-    //  weights P (S^T rows).  Padding dims read the constant chunks (ones
-    //  for dim d, zeros after it).
+    //  weights P (S^T rows).
+    //  V tail (A operand of the 16x16x32 tail products, one per pair of
+    //  k-steps 2p, 2p+1): every 16-lane group reads dims TB..TB+15, group g
+    //  the keys of k-step 2p + (g & 1) and half g >> 1, so that group g
+    //  holds contraction rows 8g..8g+7 in the order of the tail weights
+    //  (see pv).  Padding dims read the constant chunks (ones for dim d,
+    //  zeros after it).
     const int kw0 = kh * KW;  // this wave's first key within a tile
     uint32_t kaddr[C::KSTEPS];
 #pragma unroll
@@ -417,18 +433,27 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
     for (int db = 0; db < C::DBLK; ++db) {
         const int dim = 32 * db + 16 * (grp & 1) + 4 * (gi & 3);
-        if (dim < D)
-            for (int e = 0; e < NE; ++e) {
-                const int r = vkey0 + C::E_ROWS * e;
-                vaddr[db][e] = C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7);
-            }
-        else
-            for (int e = 0; e < NE; ++e) vaddr[db][e] = dim == D ? C::CONST_OFF + 16 : C::CONST_OFF;
+        for (int e = 0; e < NE; ++e) {
+            const int r = vkey0 + C::E_ROWS * e;
+            vaddr[db][e] = C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7);
+        }
+    }
+    uint32_t vtaddr = 0;  // tail: k-step pair 0, half step e = 0
+    if constexpr (C::TAIL) {
+        static_assert(!C::E_SPLIT, "tail reads step by E_ROWS rows between half k-steps");
+        const int dim = C::TB + 4 * (gi & 3);
+        const int r = kw0 + krow<C::PERM>(4 * (grp >> 1) + (gi >> 2)) + 16 * (grp & 1);
+        vtaddr = dim < D ? C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7)
+                         : (dim == D ? C::CONST_OFF + 16 : C::CONST_OFF);
     }
 
     f32x16 oacc[C::DBLK];
 #pragma unroll
     for (int db = 0; db < C::DBLK; ++db) oacc[db] = f32x16{};
+    // tail block: otail[h] = rows TB..TB+15 of O^T for queries 16h..16h+15
+    // (16x16 layout: lane l holds query 16h + (l & 15), rows TB + 4(l >> 4)
+    // + i)
+    f32x4 otail[2] = {f32x4{}, f32x4{}};
     float m_ref = -INFINITY;  // reference max of the raw dot products (this wave's keys)
     float l_run = 0.f;        // this lane's share of the running sum
     float mc = 0.f;           // m_ref * c2, the shift of the exponents
@@ -482,6 +507,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             l_run *= alpha;
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) oacc[db] *= alpha;
+            if constexpr (C::TAIL) {
+                // the tail lanes hold other queries: their own factors
+                const float a0 = __shfl(alpha, lane & 15), a1 = __shfl(alpha, 16 + (lane & 15));
+                otail[0] *= a0;
+                otail[1] *= a1;
+            }
         }
         // with no valid key yet every score is -inf and any finite shift gives 0
         mc = m_ref == -INFINITY ? 0.f : m_ref * a.c2;
@@ -503,22 +534,27 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             pb[ks] = __builtin_bit_cast(bf16x8, pw);
         }
     };
-    // V^T operands of tile t, all NKS k-steps, issued without a wait
-    auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2]) {
+    // V^T operands of tile t, all NKS k-steps, issued without a wait: the
+    // full blocks in vr, the tail (one operand per pair of k-steps) in vt
+    constexpr int NPT = C::TAIL ? NKS / 2 : 0;
+    auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2], u32x2 (&vt)[NPT > 0 ? NPT : 1][2]) {
         const uint32_t vst = lds_u32 + (uint32_t)((t % NST) * C::STAGE_BYTES);
+        if constexpr (C::TAIL) {
+            // lanes of padding dims keep reading the constant chunk
+            const bool cst = vtaddr >= (uint32_t)C::CONST_OFF;
+#pragma unroll
+            for (int pp = 0; pp < NPT; ++pp) {
+                const uint32_t a0 = vst + vtaddr + (cst ? 0u : (uint32_t)(32 * pp * C::ROWB));
+                const uint32_t a1 = vst + vtaddr + (cst ? 0u : (uint32_t)((32 * pp + C::E_ROWS) * C::ROWB));
+                vt[pp][0] = tr_read<0>(a0);
+                vt[pp][1] = tr_read<0>(a1);
+            }
+        }
         static_for<0, NKS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
             static_for<0, C::DBLK>([&](auto dbc) {
                 constexpr int db = decltype(dbc)::value;
-                if constexpr (32 * db + 31 >= D && C::DV > D) {
-                    // block with padding dims: their lanes keep reading the constant chunk
-                    static_assert(!C::E_SPLIT, "padding dims only with one V address per block");
-                    const bool cst = vaddr[db][0] >= (uint32_t)C::CONST_OFF;
-                    const uint32_t a0 = vst + vaddr[db][0] + (cst ? 0u : (uint32_t)(16 * ks * C::ROWB));
-                    const uint32_t a1 = vst + vaddr[db][0] + (cst ? 0u : (uint32_t)((16 * ks + C::E_ROWS) * C::ROWB));
-                    vr[ks][db][0] = tr_read<0>(a0);
-                    vr[ks][db][1] = tr_read<0>(a1);
-                } else if constexpr (C::E_SPLIT) {
+                if constexpr (C::E_SPLIT) {
                     vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
                     vr[ks][db][1] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][NE - 1]);
                 } else {
@@ -528,16 +564,41 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             });
         });
     };
-    // O^T += V^T P^T over the NKS k-steps
-    auto pv = [&](const u32x2 (&vr)[NKS][C::DBLK][2], const bf16x8 (&pb)[NKS]) {
+    // O^T += V^T P^T over the NKS k-steps.  Tail: for each pair of k-steps,
+    // permlane16_swap of the two steps' weights gives the 16x16x32 B
+    // operands of queries 0..15 ({x.r0, y.r0, x.r2, y.r2}: rows of 16 lanes)
+    // and 16..31 ({x.r1, y.r1, x.r3, y.r3}); group g then holds the keys of
+    // step 2p + (g & 1), half g >> 1, as the tail V^T operand does.
+    auto pv = [&](const u32x2 (&vr)[NKS][C::DBLK][2], const u32x2 (&vt)[NPT > 0 ? NPT : 1][2],
+                  const bf16x8 (&pb)[NKS]) {
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
+        for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
                 const u32x4 v4 = {vr[ks][db][0][0], vr[ks][db][0][1], vr[ks][db][1][0], vr[ks][db][1][1]};
                 oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb[ks], oacc[db],
                                                                    0, 0, 0);
             }
+            if constexpr (C::TAIL) {
+                if (ks & 1) {
+                    const u32x4 x = __builtin_bit_cast(u32x4, pb[ks - 1]), y = __builtin_bit_cast(u32x4, pb[ks]);
+                    u32x4 b0, b1;
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+                        b0[w] = r[0];
+                        b1[w] = r[1];
+                    }
+                    const int pp = ks >> 1;
+                    const u32x4 v4 = {vt[pp][0][0], vt[pp][0][1], vt[pp][1][0], vt[pp][1][1]};
+                    const bf16x8 va = __builtin_bit_cast(bf16x8, v4);
+                    otail[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b0), otail[0],
+                                                                       0, 0, 0);
+                    otail[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b1), otail[1],
+                                                                       0, 0, 0);
+                }
+            }
+        }
     };
 
     // Wait until at most the loads of the N most recently issued tiles are in
@@ -579,15 +640,16 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
         bf16x8 pb[NKS];
         weights(sc, pb);
         if constexpr (NEXT) qk(t + 1, sn);
-        u32x2 vr[NKS][C::DBLK][2];
-        read_vt(t, vr);
+        u32x2 vr[NKS][C::DBLK][2], vt[NPT > 0 ? NPT : 1][2];
+        read_vt(t, vr, vt);
         float mx = 0.f;
         if constexpr (NEXT) {
             if constexpr (MASK) mask(t + 1, sn);
             mx = row_max(sn);
         }
         lds_wait_all(vr);
-        pv(vr, pb);
+        if constexpr (C::TAIL) lds_hold(vt);
+        pv(vr, vt, pb);
         if constexpr (NEXT) update_max(mx);
     };
     using T_ = std::true_type;
@@ -695,6 +757,9 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             for (int db = 0; db < C::DBLK; ++db)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) slot[(2 + 16 * db + i) * 64 + lane] = oacc[db][i];
+            if constexpr (C::TAIL)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) slot[(2 + 16 * C::DBLK + i) * 64 + lane] = otail[i >> 2][i & 3];
         }
         // LDS only: a bare barrier, which leaves the copy loads in flight
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -709,6 +774,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
             l_run *= a0;
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) oacc[db] *= a0;
+            // tail lanes hold queries 16h + (lane & 15): factors of those queries
+            const int tq = lane & 15;
+            if constexpr (C::TAIL) {
+                otail[0] *= __shfl(a0, tq);
+                otail[1] *= __shfl(a0, 16 + tq);
+            }
 #pragma unroll
             for (int k2 = 1; k2 < KS; ++k2) {
                 const float* slot = xs + ((k2 - 1) * QB + qb) * C::XSLOT;
@@ -720,6 +791,14 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 #pragma unroll
                     for (int i = 0; i < 16; ++i)
                         oacc[db][i] = __builtin_fmaf(ak, slot[(2 + 16 * db + i) * 64 + lane], oacc[db][i]);
+                if constexpr (C::TAIL) {
+                    const float t0 = __shfl(ak, tq), t1 = __shfl(ak, 16 + tq);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        otail[0][i] = __builtin_fmaf(t0, slot[(2 + 16 * C::DBLK + i) * 64 + lane], otail[0][i]);
+                        otail[1][i] = __builtin_fmaf(t1, slot[(2 + 16 * C::DBLK + 4 + i) * 64 + lane], otail[1][i]);
+                    }
+                }
             }
             m_ref = M;
         }
@@ -732,9 +811,12 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 
     float l_tot;
     if constexpr (C::SUM_BY_MFMA) {
-        // row D of O^T: block D/32, local row lr held by lanes of half (lr/4)&1
-        constexpr int lr = D % 32, idx = 4 * (lr / 8) + (lr % 4), owner = (lr / 4) & 1;
-        l_tot = __shfl(oacc[D / 32][idx], c + 32 * owner);
+        // row D of O^T: tail row lr, held (16x16 layout) by lane 16(lr/4) + q%16
+        // of otail[q/16], register lr%4
+        constexpr int lr = D - C::TB;
+        const float s0 = __shfl(otail[0][lr % 4], 16 * (lr / 4) + (c & 15));
+        const float s1 = __shfl(otail[1][lr % 4], 16 * (lr / 4) + (c & 15));
+        l_tot = c < 16 ? s0 : s1;
     } else {
         l_tot = halves_sum(l_run);
     }
@@ -789,6 +871,34 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
                 __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
             }
         }
+    if constexpr (C::TAIL) {
+        // tail dims TB + 4(lane >> 4) .. +3 of queries 16h + (lane & 15),
+        // with those queries' weights
+        const int dim = C::TB + 4 * (lane >> 4);
+        const float wn[2] = {__shfl(w_new, lane & 15), __shfl(w_new, 16 + (lane & 15))};
+        const float wp[2] = {__shfl(w_prev, lane & 15), __shfl(w_prev, 16 + (lane & 15))};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int qr = qt * C::BM + qb * 32 + 16 * h + (lane & 15);
+            if (dim < D) {
+                const uint32_t o = qr < a.Nq ? (uint32_t)qr * rowb + headb + 2 * dim : kOOB;
+                float y[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) y[e] = otail[h][e] * wn[h];
+                if (wp[h] != 0.f) {
+                    const u32x2 pv = __builtin_amdgcn_raw_buffer_load_b64(ro, o, 0, 0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t hw = pv[e >> 1];
+                        const float x = __uint_as_float((e & 1) ? (hw & 0xffff0000u) : (hw << 16));
+                        y[e] = __builtin_fmaf(wp[h], x, y[e]);
+                    }
+                }
+                const u32x2 w = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+                __builtin_amdgcn_raw_buffer_store_b64(w, ro, o, 0, 0);
+            }
+        }
+    }
     if (lse_base && hf == 0 && qvalid) lse_base[lidx] = lse_out;
     if constexpr (PATCH) copy_rest();
 }
