@@ -180,25 +180,33 @@ int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n,
                    int64_t head_dim, int32_t dtype);
 
 /*
- * Key-split forms of xdit_chunk_attn and xdit_patch_attn_ranges, for query
- * counts that leave most of the 256 CUs idle (few query tiles per head).
- * Each query tile's K/V sweep is cut into `splits` consecutive parts that run
- * as separate workgroups; every part writes its partial output and
- * log-sum-exp into the workspace, and the log-sum-exp merge of Section 4.1.1
- * (the same arithmetic as xdit_lse_merge) combines them into out and lse.
- * The results equal the unsplit call's up to the bf16 rounding of the
- * partials.
+ * Key-split forms of xdit_chunk_attn and xdit_patch_attn_ranges, for launches
+ * whose query tiles (128 rows each, per batch and head) leave CUs of the 256
+ * idle: too few query tiles, or a last round of workgroups that is nearly
+ * empty.  The K/V sweep of a query tile is cut into consecutive parts that
+ * run as separate workgroups; each part writes its partial output and
+ * log-sum-exp (float32) into the workspace, and a fix-up launch combines the
+ * parts of each cut sweep by the log-sum-exp merge of Section 4.1.1 (the
+ * same arithmetic as xdit_lse_merge) into out and lse.  The results equal
+ * the unsplit call's up to float32 rounding of the merge.
  *
  *   splits     1 .. XDIT_MAX_SPLITS, or <= 0 to let the library choose
- *              (fewest rounds of workgroups over the CUs per unit of work,
- *              at least four 128-key tiles per part); 1 = the unsplit call
+ *              splits > 1: every sweep is cut into `splits` even parts;
+ *              1: the unsplit call;
+ *              <= 0: the library's choice from a time model of the launch:
+ *              no cut, every sweep cut into s even parts (few query tiles),
+ *              or the query tiles of the full rounds of workgroups swept
+ *              whole and each of the r left over cut into min(16, 256 / r)
+ *              parts (a nearly empty last round); a cut is taken only when
+ *              the model saves at least 10 %
  *   workspace  device memory of at least xdit_split_workspace_bytes(...)
  *              bytes for the same sizes and splits, 256-byte aligned, not
- *              overlapping any argument; unused (may be NULL) when no split
+ *              overlapping any argument; unused (may be NULL) when no cut
  *              happens.  Its contents on entry do not matter.
- * float32 calls run unsplit.  Other arguments as for the unsplit calls.
- * The split sweep and the merge are two launches on the calling thread's
- * stream.
+ * xdit_split_workspace_bytes returns 0 when the sizes lead to no cut, -1 for
+ * sizes or splits the calls reject.  float32 calls run unsplit.  Other
+ * arguments as for the unsplit calls.  The sweep and the fix-up are two
+ * launches on the calling thread's stream.
  */
 int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
                                    int64_t head_dim, int32_t dtype, int32_t splits);

@@ -131,6 +131,9 @@ struct Cfg {
     static constexpr int XSLOT = 64 * (2 + 16 * DBLK + (TAIL ? 8 : 0));  // floats
     static constexpr int X_BYTES = 4 * QB * (KS - 1) * XSLOT;
     static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES > X_BYTES ? NSTAGE * STAGE_BYTES : X_BYTES;
+    // partial (O, LSE) of one query tile: O as float4 chunks [D/4][BM],
+    // then the LSE of the BM rows
+    static constexpr int SLOT_FLOATS = BM * (D + 1);
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
     static_assert(!TAIL || (D - TB <= 15 && D - TB > 0 && KW % 32 == 0), "tail block: dims TB..D-1, then the ones row");
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
@@ -155,10 +158,21 @@ struct Args {
     int sa0, sn0, sa1, sn1;      // tiles [sa, sa + sn) hold rows of fresh range 0 / 1
     float c2;  // softmax scale * log2(e)
     int accum;  // merge into the running (out, lse) instead of overwriting them
-    // key splits: split sp of a query tile sweeps K/V tiles [T*sp/S, T*(sp+1)/S)
-    // and writes its partial (O, LSE) at out + sp*out_split, lse + sp*lse_split
-    int splits;
-    int64_t out_split, lse_split;  // elements
+    // Work partition.  A pair is one query tile of one (batch, head), pair
+    // index bh * q_tiles + qt; its sweep is T K/V tiles (T >= 1); the units
+    // (pair, tile) are counted in pair-major order, pairs * T of them.  In a
+    // partitioned launch the first G1 workgroups sweep pairs 0..G1-1 whole,
+    // one each; the units of the other pairs, [G1 * T, units), are split
+    // into G2 = gridDim.x - G1 contiguous ranges, one per further
+    // workgroup.  A workgroup walks its range as segments, one per pair it
+    // touches.  A segment over a whole sweep writes out (and lse); any other
+    // writes its normalised partial O and its LSE to slot j (the range's
+    // first segment) or G2 + j (its last) of `part`, j = the range index,
+    // for the fix-up.
+    int T;
+    int64_t units;
+    int G1;
+    float* part;
 };
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
@@ -256,27 +270,31 @@ __device__ __forceinline__ float halves_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QB, int KS, int KW, bool PATCH>
-__global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
+// One segment: K/V tiles [tile0, tile0 + nt) of the sweep of pair `pair`;
+// pslot: where its partial goes, nullptr for a whole sweep.
+template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS>
+__device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, int pair, int tile0, int nt,
+                                             float* pslot) {
     using C = Cfg<D, QB, KS, KW>;
     constexpr int NT = C::THREADS, BN = C::BN, NST = C::NSTAGE, NKB = C::NKB, NKS = C::NKS;
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
 
-    const int tid = threadIdx.x;
+    // In a partitioned launch the thread index is made opaque to the
+    // compiler, so that the lane's addresses are derived anew in each segment
+    // rather than kept live across segments (which made the sweep spill).
+    int tid = threadIdx.x;
+    if constexpr (PARTS) asm volatile("" : "+v"(tid));
     const int lane = tid & 63, wave = tid >> 6;
     const int c = lane & 31, hf = lane >> 5;
     const int qb = wave % QB, kh = wave / QB;  // query block, key split
 
-    const int logical = xcd_remap(blockIdx.x, gridDim.x);
-    const int qt = logical % a.q_tiles;
-    const int sp = (logical / a.q_tiles) % a.splits;
-    const int bh = logical / a.q_tiles / a.splits;
-    uint16_t* const out_base = a.out + sp * a.out_split;
-    float* const lse_base = a.lse ? a.lse + sp * a.lse_split : nullptr;
-    // this split's K/V tiles; t counts them from 0, tile tb + t of the sequence
+    const int qt = pair % a.q_tiles, bh = pair / a.q_tiles;
+    uint16_t* const out_base = a.out;
+    float* const lse_base = a.lse;
+    // this segment's K/V tiles; t counts them from 0, tile tb + t of the
+    // sequence (none past the end: with Nk = 0 the one unit has no tile)
     const int all_tiles = (a.Nk + BN - 1) / BN;
-    const int tb = (int)((int64_t)all_tiles * sp / a.splits);
-    const int ntiles = (int)((int64_t)all_tiles * (sp + 1) / a.splits) - tb;
+    const int tb = tile0;
+    const int ntiles = max(0, min(nt, all_tiles - tile0));
     const int hh = bh % a.H, b = bh / a.H;
     const uint32_t rowb = (uint32_t)a.H * D * 2;  // bytes between consecutive rows in memory
     const uint32_t headb = (uint32_t)hh * D * 2;  // byte offset of this head in a row
@@ -708,9 +726,10 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     // operations hold up none of the sweep's waits, and the first batch's
     // loads are in flight during the key-split merge and the output.
     constexpr int CU = 4;  // 16-byte chunks per lane and batch
-    const int cshare = qt * a.splits + sp, cshares = a.q_tiles * a.splits;
-    const int cr0 = (int)((int64_t)F * cshare / cshares);
-    const int cn = ((int)((int64_t)F * (cshare + 1) / cshares) - cr0) * C::CH;  // chunks of the share
+    // the share of this segment's units among the head's q_tiles * T
+    const int64_t hu = (int64_t)a.q_tiles * a.T, u0 = (int64_t)qt * a.T + tile0;
+    const int cr0 = (int)((int64_t)F * u0 / hu);
+    const int cn = ((int)((int64_t)F * (u0 + nt) / hu) - cr0) * C::CH;  // chunks of the share
     uint32_t cd[CU];
     u32x4 ck[CU], cv[CU];
     // loads of batch e0 .. e0 + CU*NT - 1; chunks past the share use the
@@ -823,6 +842,31 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     constexpr float kLn2 = 0.69314718055994531f;
     const float lse_new = l_tot > 0.f ? (m_ref * a.c2 + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (pslot != nullptr) {
+        // partial sweep: normalised O and the LSE in float32, for the
+        // fix-up; chunk k4 (dims 4k4..4k4+3) of tile row r at float4 k4*BM + r
+        f32x4* po = (f32x4*)pslot;
+        const int r = qb * 32 + c;
+#pragma unroll
+        for (int db = 0; db < C::DBLK; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const f32x4 y = {oacc[db][4 * g] * inv, oacc[db][4 * g + 1] * inv, oacc[db][4 * g + 2] * inv,
+                                 oacc[db][4 * g + 3] * inv};
+                po[(8 * db + 2 * g + hf) * C::BM + r] = y;
+            }
+        if constexpr (C::TAIL) {
+            const int k4 = C::TB / 4 + (lane >> 4);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float iv = __shfl(inv, 16 * h + (lane & 15));
+                if (4 * k4 < D) po[k4 * C::BM + qb * 32 + 16 * h + (lane & 15)] = otail[h] * iv;
+            }
+        }
+        if (hf == 0) pslot[C::BM * D + r] = lse_new;
+        if constexpr (PATCH) copy_rest();
+        return;
+    }
     const int64_t lidx = ((int64_t)b * a.H + hh) * a.Nq + qrow;
     // Merge into a running (out, lse) (the ring's accumulation over chunks,
     // Section 4.1.1): weights e^{lse_prev - L} and e^{lse_new - L} with
@@ -903,6 +947,154 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
     if constexpr (PATCH) copy_rest();
 }
 
+// One workgroup per query tile (PARTS = false: workgroup L sweeps pair L
+// whole), or a partitioned launch (PARTS = true, see Args).  Workgroup ids
+// are remapped per group (whole sweeps, cut ranges) so that neighbouring
+// pairs share an XCD; G1 is a multiple of 8, so both groups start on XCD 0.
+template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS>
+__global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
+    using C = Cfg<D, QB, KS, KW>;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
+    if constexpr (!PARTS) {
+        attn_segment<D, QB, KS, KW, PATCH, false>(a, lds, xcd_remap(blockIdx.x, gridDim.x), 0, a.T, nullptr);
+        return;
+    }
+    const int G2 = gridDim.x - a.G1;
+    int64_t ub, ue;
+    int j = 0;
+    if ((int)blockIdx.x < a.G1) {
+        ub = (int64_t)xcd_remap(blockIdx.x, a.G1) * a.T;
+        ue = ub + a.T;
+    } else {
+        j = xcd_remap(blockIdx.x - a.G1, G2);
+        const int64_t base = (int64_t)a.G1 * a.T, rem = a.units - base;
+        ub = base + rem * j / G2;
+        ue = base + rem * (j + 1) / G2;
+    }
+    for (int64_t u = ub; u < ue;) {
+        const int pair = (int)(u / a.T);
+        const int t0 = (int)(u - (int64_t)pair * a.T);
+        const int nt = (int)min((int64_t)(a.T - t0), ue - u);
+        float* slot = t0 == 0 && nt == a.T ? nullptr : a.part + (int64_t)(u == ub ? j : G2 + j) * C::SLOT_FLOATS;
+        if (u != ub) __syncthreads();  // the previous segment is done with LDS
+        attn_segment<D, QB, KS, KW, PATCH, true>(a, lds, pair, t0, nt, slot);
+        u += nt;
+    }
+}
+
+// Fix-up of a launch whose partition cut some sweeps: the partials of every
+// range that meets a cut sweep are merged (the LSE merge of Section 4.1.1
+// over the key parts) into out and lse, by workgroups (x, rb) for tile rows
+// 16rb..16rb+15.  When each of the cut query tiles is cut into s_al even
+// parts (s_al > 0), workgroup x handles the x-th of them, whose parts are
+// ranges x*s_al .. x*s_al + s_al - 1.  Otherwise workgroup x handles the
+// boundary between ranges x and x + 1 when it falls inside a sweep and is
+// the first boundary inside it, and finds the ranges that meet that sweep.
+// Thread t: row 16rb + t % 16, dim chunks t / 16, t / 16 + 16, ...
+struct FixArgs {
+    uint16_t* out;
+    float* lse;
+    const float* part;
+    int B, H, Nq, q_tiles, T, G2, s_al;
+    int64_t base, rem;  // the cut ranges split units [base, base + rem)
+};
+
+constexpr int kMaxParts = kMaxSweepParts;
+constexpr int kFixRows = 16;  // tile rows per fix-up workgroup
+
+template <int D, int BM>
+__global__ __launch_bounds__(256) void fixup_kernel(FixArgs a) {
+    // thread 0 finds the sweep and its parts (64-bit index arithmetic) and
+    // hands them to the others through LDS
+    __shared__ int64_t sh_pair;
+    __shared__ int64_t sh_slot[kMaxParts];
+    __shared__ int sh_n;
+    if (threadIdx.x == 0 && a.s_al > 0) {
+        // part i of cut sweep x is range x*s + i: units T*i/s .. T*(i+1)/s of
+        // the sweep (empty when that is)
+        const int x = blockIdx.x, sa = a.s_al;
+        int n = 0;
+        for (int i = 0; i < sa && n < kMaxParts; ++i)
+            if (a.T * (i + 1) / sa > a.T * i / sa) sh_slot[n++] = (int64_t)x * sa + i;
+        sh_pair = a.base / a.T + x;
+        sh_n = n;
+    } else if (threadIdx.x == 0) {
+        const int g = blockIdx.x + 1;
+        const int64_t G = a.G2, T = a.T;
+        auto ub = [&](int64_t w) { return a.base + a.rem * w / G; };
+        const int64_t bg = ub(g), P = bg / T, pu0 = P * T, pu1 = pu0 + T;
+        int n = 0;
+        // only a boundary inside a sweep, and the first one inside it
+        if (bg != pu0 && ub(g - 1) <= pu0) {
+            // the parts: ranges w >= g - 1 that are non-empty and meet
+            // [pu0, pu1); slot w if the part is w's first segment, G + w
+            // otherwise (the host bounds their number by kMaxParts)
+            int64_t w = g - 1, b0 = ub(w);
+            while (w < G && n < kMaxParts) {
+                const int64_t b1 = ub(w + 1);
+                if (b0 >= pu1) break;
+                if (b1 > b0) sh_slot[n++] = b0 >= pu0 ? w : G + w;
+                ++w;
+                b0 = b1;
+            }
+        }
+        sh_pair = P;
+        sh_n = n;
+    }
+    __syncthreads();
+    const int n = sh_n;
+    if (n == 0) return;
+    const int64_t P = sh_pair;
+    const int qt = (int)(P % a.q_tiles), bh = (int)(P / a.q_tiles), hh = bh % a.H, b = bh / a.H;
+    const int r = kFixRows * blockIdx.y + (int)threadIdx.x % kFixRows, dg = (int)threadIdx.x / kFixRows;
+    const int qrow = qt * BM + r;
+    if (qrow >= a.Nq) return;
+    constexpr int SLOT = BM * (D + 1);
+    // every load of the thread issued up front (parts beyond n predicated
+    // off): the merge is latency-bound otherwise
+    const float* base[kMaxParts];
+    float lw[kMaxParts];
+#pragma unroll
+    for (int i = 0; i < kMaxParts; ++i) {
+        base[i] = a.part + (i < n ? sh_slot[i] : 0) * SLOT;
+        lw[i] = i < n ? base[i][BM * D + r] : -INFINITY;
+    }
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    constexpr int C4 = D / 4, NG = 256 / kFixRows, PER = (C4 + NG - 1) / NG;
+    f32x4_t x[kMaxParts][PER];
+#pragma unroll
+    for (int i = 0; i < kMaxParts; ++i)
+#pragma unroll
+        for (int kk = 0; kk < PER; ++kk)
+            if (i < n && dg + NG * kk < C4) x[i][kk] = ((const f32x4_t*)base[i])[(dg + NG * kk) * BM + r];
+    float M = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kMaxParts; ++i) M = fmaxf(M, lw[i]);
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxParts; ++i) sum += lw[i] == -INFINITY ? 0.f : __expf(lw[i] - M);
+    const float L = M == -INFINITY ? -INFINITY : M + __logf(sum);
+    // O = sum_i exp(lse_i - L) O_i over this thread's dim chunks
+    f32x4_t acc[PER];
+#pragma unroll
+    for (int kk = 0; kk < PER; ++kk) acc[kk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kMaxParts; ++i) {
+        const float w = lw[i] == -INFINITY ? 0.f : __expf(lw[i] - L);
+#pragma unroll
+        for (int kk = 0; kk < PER; ++kk)
+            if (i < n && dg + NG * kk < C4) acc[kk] += w * x[i][kk];
+    }
+    uint16_t* orow = a.out + (((int64_t)b * a.Nq + qrow) * a.H + hh) * D;
+#pragma unroll
+    for (int kk = 0; kk < PER; ++kk)
+        if (dg + NG * kk < C4)
+            ((u32x2_t*)orow)[dg + NG * kk] =
+                u32x2_t{pack_bf16x2(acc[kk][0], acc[kk][1]), pack_bf16x2(acc[kk][2], acc[kk][3])};
+    if (a.lse && dg == 0) a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = L;
+}
+
 template <int D, int QB, int KS, int KW, bool PATCH>
 hipError_t launch(const AttnParams& p, hipStream_t s) {
     using C = Cfg<D, QB, KS, KW>;
@@ -930,16 +1122,48 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.sa1 = p.len1 > 0 ? p.off1 / C::BN : 0;
     a.sn1 = p.len1 > 0 ? (p.off1 + p.len1 + C::BN - 1) / C::BN - a.sa1 : 0;
     a.q_tiles = (p.Nq + C::BM - 1) / C::BM;
-    a.splits = p.splits > 1 ? p.splits : 1;
-    a.out_split = p.out_split;
-    a.lse_split = p.lse_split;
     a.c2 = (float)(1.4426950408889634 / sqrt((double)D));
     a.accum = p.accum;
-    const int64_t blocks = (int64_t)a.q_tiles * a.splits * p.H * p.B;
-    if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH>), dim3((unsigned)blocks), dim3(C::THREADS),
-                       0, s, a);
-    return hipGetLastError();
+    a.T = max(1, (p.Nk + C::BN - 1) / C::BN);
+    const int64_t pairs = (int64_t)a.q_tiles * p.H * p.B;
+    a.units = pairs * a.T;
+    a.G1 = (int)p.whole;
+    a.part = p.part;
+    if (pairs == 0) return hipSuccess;
+    const bool parts = p.parts > 0;
+    if (parts && p.accum) return hipErrorInvalidValue;  // the fix-up does not merge into a running state
+    if (!parts) {
+        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, false>), dim3((unsigned)pairs), dim3(C::THREADS),
+                           0, s, a);
+        return hipGetLastError();
+    }
+    if constexpr (C::BM != kPartSlotRows) {
+        return hipErrorInvalidValue;  // only the 128-row shape runs partitioned launches (slot layout)
+    } else {
+        if (p.whole < 0 || p.whole > pairs || p.whole % 8 != 0) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, true>), dim3((unsigned)(p.whole + p.parts)),
+                           dim3(C::THREADS), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || p.parts < 2) return e;
+        // merge the partials of the cut sweeps
+        FixArgs f;
+        f.out = a.out;
+        f.lse = a.lse;
+        f.part = a.part;
+        f.B = p.B;
+        f.H = p.H;
+        f.Nq = p.Nq;
+        f.q_tiles = a.q_tiles;
+        f.T = a.T;
+        f.G2 = (int)p.parts;
+        f.base = p.whole * a.T;
+        f.rem = a.units - f.base;
+        const int64_t cut = pairs - p.whole;  // query tiles in the cut ranges
+        f.s_al = p.parts % cut == 0 ? (int)(p.parts / cut) : 0;
+        const int64_t gx = f.s_al > 0 ? cut : p.parts - 1;
+        hipLaunchKernelGGL((fixup_kernel<D, C::BM>), dim3((unsigned)gx, C::BM / kFixRows), dim3(256), 0, s, f);
+        return hipGetLastError();
+    }
 }
 
 // Shapes of 8-wave workgroup.  "Wide": 128 query rows as 4 query blocks x 2
@@ -972,7 +1196,7 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
     } else {
         const int forced = forced_shape();
         // split keys fill the GPU by themselves: 128-row query tiles
-        if (forced == 1 || p.splits > 1) return launch<D, 4, 2, 64, PATCH>(p, s);
+        if (forced == 1 || p.parts > 0) return launch<D, 4, 2, 64, PATCH>(p, s);
         if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
         const int64_t bh = (int64_t)p.B * p.H;
         const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;

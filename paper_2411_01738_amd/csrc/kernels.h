@@ -25,10 +25,16 @@ struct AttnParams {
     int off0, len0;       // first fresh range
     int off1, len1;       // second fresh range (len1 == 0: none); disjoint from the first
     int accum;            // merge into the running (out, lse) instead of overwriting them
-    // key splits (bf16 only): split s writes its partial at out + s*out_split
-    // and lse + s*lse_split (elements); splits <= 1: no split
-    int splits;
-    int64_t out_split, lse_split;
+    // Work partition (bf16 only; 128-row query tiles).  parts = 0: one
+    // workgroup per query tile.  parts > 0: `whole` workgroups (a multiple
+    // of 8) sweep the first `whole` query tiles whole, and the (query tile,
+    // K/V tile) units of the others are cut into `parts` contiguous ranges,
+    // one workgroup each; partials of cut sweeps go to `part`
+    // (kPartSlotRows * (D + 1) floats per slot; slots 0..parts-1, and
+    // parts..2*parts-1 when ranges may cross query tiles) and a fix-up
+    // launch merges them.
+    int64_t whole, parts;
+    float* part;
 };
 
 struct MergeParams {
@@ -52,6 +58,8 @@ struct UpdateParams {
 };
 
 constexpr int kMaxPartials = 64;
+constexpr int kPartSlotRows = 128;  // query rows of a partitioned launch's tile
+constexpr int kMaxSweepParts = 17;  // most partition ranges one sweep may meet
 
 hipError_t launch_attn_bf16(const AttnParams& p, hipStream_t s);
 hipError_t launch_attn_f32(const AttnParams& p, hipStream_t s);

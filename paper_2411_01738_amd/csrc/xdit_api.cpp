@@ -2,6 +2,7 @@
 // the per-thread stream and error message, and dispatch to the HIP kernels.
 // Every check runs before any HIP call, so a rejected call touches neither the
 // device nor the caller's buffers.
+#include <cmath>
 #include "../../include/xdit.h"
 
 #include <hip/hip_runtime.h>
@@ -10,6 +11,8 @@
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <map>
 #include <mutex>
@@ -122,90 +125,121 @@ struct SplitArgs {
 };
 
 static constexpr int kCUs = 256;
-static constexpr int kSplitRows = 128;  // query rows per workgroup when keys are split
+static constexpr int kPartRows = xdit::kPartSlotRows;  // query rows per tile of a partitioned launch
 
 static int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
 
-static int64_t split_ws_bytes(int64_t batch, int64_t q_len, int64_t heads, int64_t head_dim, int es, int s) {
-    return align256((int64_t)s * batch * q_len * heads * head_dim * es) + (int64_t)s * batch * heads * q_len * 4;
+// Query tiles of a partitioned launch (128 rows) over the batch and heads.
+static int64_t part_pairs(int64_t batch, int64_t q_len, int64_t heads) {
+    return (q_len + kPartRows - 1) / kPartRows * batch * heads;
 }
 
-// Key splits for a launch of `work` query tiles over `tiles` K/V tiles.
-// Time model in units of one K/V tile of one workgroup: each round of
-// workgroups over the CUs costs a fixed ~4 tiles (prologue, pipeline fill,
-// epilogue) plus its sweep, and a split adds the merge pass (~2 tiles).  A
-// split is taken only when the model saves at least 10 %: with measured
-// per-workgroup overheads, splitting pays only when whole rounds are
-// saved (a tile count well below the CU count).
-static int pick_splits(int64_t work, int64_t tiles) {
-    auto cost = [&](int s) {
-        const double rounds = (double)((work * s + kCUs - 1) / kCUs);
-        return rounds * (4.0 + (double)tiles / s) + (s > 1 ? 2.0 : 0.0);
-    };
-    int best = 1;
-    double best_cost = cost(1);
-    for (int s = 2; s <= XDIT_MAX_SPLITS && tiles >= 4 * s; ++s)
-        if (cost(s) < best_cost) {
-            best_cost = cost(s);
-            best = s;
+// A work partition of a bf16 launch (see xdit::AttnParams): `whole`
+// workgroups sweep query tiles whole, `parts` workgroups take the cut ranges
+// of the rest; parts = 0: one workgroup per query tile.
+struct Partition {
+    int64_t whole = 0, parts = 0;
+};
+
+// Workspace of a partitioned launch: one partial slot (O and LSE in float32)
+// per cut range, two when ranges may cross query tiles.
+static int64_t part_ws_bytes(const Partition& pt, int64_t pairs, int64_t head_dim) {
+    if (pt.parts <= 0) return 0;
+    const int64_t slots = pt.parts % (pairs - pt.whole) == 0 ? pt.parts : 2 * pt.parts;
+    return align256(slots * kPartRows * (head_dim + 1) * 4);
+}
+
+// The library's partition for `pairs` query tiles over kv_len keys.  Time
+// model in units of one 128-key tile of one workgroup: a workgroup's sweep
+// (or part of one) costs a fixed ~5 tiles (prologue, pipeline fill,
+// epilogue) plus its tiles; each round of workgroups over the CUs costs its
+// longest member; cut sweeps add the fix-up launch (~3 tiles).  Candidates:
+//   * one workgroup per query tile (of 128 rows, or of 64 at d <= 72);
+//   * every sweep cut into s even parts (s = 2..XDIT_MAX_SPLITS), for query
+//     tiles that leave CUs idle;
+//   * the query tiles of the full rounds whole and each of the r left over
+//     cut into s = min(16, 256 / r) parts, so that the last round is full
+//     (K/V reuse among the query tiles of one head is kept in the rounds of
+//     whole sweeps).
+// A partition is taken only when the model saves at least 10 %.
+// XDIT_PARTITION=balanced instead cuts the whole launch into 256 equal
+// ranges (ranges cross query tiles; it loses the K/V reuse, so it is never
+// chosen; tests use it), XDIT_PARTITION=none forces no partition.
+static Partition pick_parts(int64_t pairs, int64_t kv_len, int64_t head_dim) {
+    Partition none;
+    const char* force = getenv("XDIT_PARTITION");
+    if (force && strcmp(force, "none") == 0) return none;
+    const int64_t bn = head_dim > 96 ? 64 : 128;  // kernel K/V tile
+    const int64_t T = (kv_len + bn - 1) / bn > 1 ? (kv_len + bn - 1) / bn : 1;
+    if (force && strcmp(force, "balanced") == 0) {
+        // every sweep may meet at most kMaxSweepParts ranges
+        if (pairs * T / kCUs * (xdit::kMaxSweepParts - 1) >= T) {
+            Partition b;
+            b.parts = kCUs;
+            return b;
         }
-    return best_cost < 0.9 * cost(1) ? best : 1;
+        return none;
+    }
+    const double t = (double)((kv_len + 127) / 128 > 1 ? (kv_len + 127) / 128 : 1);
+    const double ovh = 5.0, fix = 3.0;
+    auto rounds = [](int64_t n) { return (double)((n + kCUs - 1) / kCUs); };
+    // unpartitioned: 128-row query tiles, or at d <= 72 64-row ones (twice
+    // the workgroups, half the work per tile)
+    double plain = rounds(pairs) * (t + ovh);
+    if (head_dim <= 72 && rounds(2 * pairs) * (t / 2 + ovh) < plain) plain = rounds(2 * pairs) * (t / 2 + ovh);
+    double best = plain;
+    Partition pick;
+    for (int s = 2; s <= XDIT_MAX_SPLITS && t >= 4.0 * s; ++s) {
+        const double c = rounds(pairs * s) * (ovh + t / s) + fix;
+        if (c < best) {
+            best = c;
+            pick.whole = 0;
+            pick.parts = pairs * s;
+        }
+    }
+    const int64_t full = pairs / kCUs * kCUs, r = pairs - full;
+    const int64_t s = r > 0 ? (kCUs / r < XDIT_MAX_SPLITS ? kCUs / r : XDIT_MAX_SPLITS) : 0;
+    if (full > 0 && s >= 2 && t >= 2.0 * s) {
+        const double c = (double)(full / kCUs) * (t + ovh) + (ovh + t / s) + fix;
+        if (c < best) {
+            best = c;
+            pick.whole = full;
+            pick.parts = r * s;
+        }
+    }
+    return best < 0.9 * plain ? pick : none;
 }
 
-// Resolve the split count and check the workspace; returns XDIT_OK and sets
-// *s_out (1 = no split).
-static int resolve_splits(const char* fn, const SplitArgs& sa, int32_t dtype, int64_t batch, int64_t q_len,
-                   int64_t kv_len, int64_t heads, int64_t head_dim, int* s_out) {
+// Resolve the partition and check the workspace; returns XDIT_OK and sets
+// *pt_out.
+static int resolve_parts(const char* fn, const SplitArgs& sa, int32_t dtype, int64_t batch, int64_t q_len,
+                         int64_t kv_len, int64_t heads, int64_t head_dim, Partition* pt_out) {
     if (sa.splits > XDIT_MAX_SPLITS)
         return fail(XDIT_ERR_RANGE, "%s: splits = %d above %d", fn, sa.splits, XDIT_MAX_SPLITS);
-    int s = sa.splits;
-    if (dtype != XDIT_BF16) s = 1;  // the float32 path is not split
-    if (s <= 0) {
-        const int64_t work = (q_len + kSplitRows - 1) / kSplitRows * batch * heads;
-        const int64_t tiles = (kv_len + 127) / 128;
-        s = pick_splits(work, tiles);
+    Partition pt;
+    const int64_t pairs = part_pairs(batch, q_len, heads);
+    if (dtype == XDIT_BF16 && pairs > 0) {  // the float32 path is not partitioned
+        if (sa.splits > 1) pt.parts = pairs * sa.splits;
+        else if (sa.splits <= 0) pt = pick_parts(pairs, kv_len, head_dim);
     }
-    if (s > 1) {
-        const int64_t need = split_ws_bytes(batch, q_len, heads, head_dim, esize_of(dtype), s);
+    if (pt.parts > 0) {
+        const int64_t need = part_ws_bytes(pt, pairs, head_dim);
         if (sa.workspace == nullptr || sa.workspace_bytes < need)
-            return fail(XDIT_ERR_RANGE, "%s: workspace of %lld bytes, %d splits need %lld", fn,
-                        (long long)sa.workspace_bytes, s, (long long)need);
+            return fail(XDIT_ERR_RANGE, "%s: workspace of %lld bytes, the partition needs %lld", fn,
+                        (long long)sa.workspace_bytes, (long long)need);
         if ((uintptr_t)sa.workspace & 255u) return fail(XDIT_ERR_LAYOUT, "%s: workspace not 256-byte aligned", fn);
     }
-    *s_out = s;
+    *pt_out = pt;
     return XDIT_OK;
 }
 
-// Launch an attention whose keys are split s ways: partials into the
-// workspace, then their log-sum-exp merge into out / lse.
-static hipError_t launch_split(xdit::AttnParams p, int s, void* workspace, int32_t dtype) {
-    const int64_t ob = (int64_t)p.B * p.Nq * p.H * p.D * esize_of(dtype);
-    void* out = p.out;
-    float* lse = p.lse;
-    p.splits = s;
-    p.out = workspace;
-    p.lse = (float*)((char*)workspace + align256((int64_t)s * ob));
-    p.out_split = (int64_t)p.B * p.Nq * p.H * p.D;
-    p.lse_split = (int64_t)p.B * p.H * p.Nq;
-    hipError_t e = xdit::launch_attn_bf16(p, g_stream);
-    if (e != hipSuccess) return e;
-    const void* outs[XDIT_MAX_SPLITS];
-    const float* lses[XDIT_MAX_SPLITS];
-    for (int r = 0; r < s; ++r) {
-        outs[r] = (const char*)workspace + r * ob;
-        lses[r] = p.lse + r * p.lse_split;
-    }
-    xdit::MergeParams m{};
-    m.outs = outs;
-    m.lses = lses;
-    m.n = s;
-    m.out = out;
-    m.lse_out = lse;
-    m.B = p.B;
-    m.Nq = p.Nq;
-    m.H = p.H;
-    m.D = p.D;
-    return xdit::launch_merge_bf16(m, g_stream);
+// Launch a partitioned attention: the sweep workgroups, then the fix-up of
+// cut sweeps (both inside launch_attn_bf16).
+static hipError_t launch_parts(xdit::AttnParams p, const Partition& pt, void* workspace) {
+    p.whole = pt.whole;
+    p.parts = pt.parts;
+    p.part = (float*)workspace;
+    return xdit::launch_attn_bf16(p, g_stream);
 }
 
 static int chunk_impl(const char* fn, const void* q, const void* k, const void* v, void* out,
@@ -229,10 +263,10 @@ static int chunk_impl(const char* fn, const void* q, const void* k, const void* 
         XDIT_TRY(check_no_overlap(sl, *s));
     }
     XDIT_TRY(check_no_overlap(sl, so));
-    int splits = 1;
-    XDIT_TRY(resolve_splits(fn, sa, dtype, batch, q_len, kv_len, heads, head_dim, &splits));
-    if (splits > 1) {
-        const Span sw{sa.workspace, split_ws_bytes(batch, q_len, heads, head_dim, (int)es, splits),
+    Partition parts;
+    XDIT_TRY(resolve_parts(fn, sa, dtype, batch, q_len, kv_len, heads, head_dim, &parts));
+    if (parts.parts > 0) {
+        const Span sw{sa.workspace, part_ws_bytes(parts, part_pairs(batch, q_len, heads), head_dim),
                       "workspace"};
         for (const Span* s : {&sq, &sk, &sv, &so, &sl}) XDIT_TRY(check_no_overlap(sw, *s));
     }
@@ -250,7 +284,7 @@ static int chunk_impl(const char* fn, const void* q, const void* k, const void* 
     p.Nk = (int)kv_len;
     p.D = (int)head_dim;
     p.accum = accum;
-    if (splits > 1) return hip_status(launch_split(p, splits, sa.workspace, dtype), fn);
+    if (parts.parts > 0) return hip_status(launch_parts(p, parts, sa.workspace), fn);
     const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
                                             : xdit::launch_attn_f32(p, g_stream);
     return hip_status(e, fn);
@@ -335,10 +369,11 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
         XDIT_TRY(check_no_overlap(sl, *s));
     }
     XDIT_TRY(check_no_overlap(sl, so));
-    int splits = 1;
-    XDIT_TRY(resolve_splits(fn, sa, dtype, batch, q_len, seq_len, heads, head_dim, &splits));
-    if (splits > 1) {
-        const Span sw{sa.workspace, split_ws_bytes(batch, q_len, heads, head_dim, es, splits), "workspace"};
+    Partition parts;
+    XDIT_TRY(resolve_parts(fn, sa, dtype, batch, q_len, seq_len, heads, head_dim, &parts));
+    if (parts.parts > 0) {
+        const Span sw{sa.workspace, part_ws_bytes(parts, part_pairs(batch, q_len, heads), head_dim),
+                      "workspace"};
         for (const Span* s : {&sb, &sk, &sv, &sq, &so, &sl}) XDIT_TRY(check_no_overlap(sw, *s));
     }
     if (batch == 0 || heads == 0) return XDIT_OK;
@@ -389,7 +424,7 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
     p.len0 = (int)len[0];
     p.off1 = (int)off[1];
     p.len1 = (int)len[1];
-    if (splits > 1) return hip_status(launch_split(p, splits, sa.workspace, dtype), fn);
+    if (parts.parts > 0) return hip_status(launch_parts(p, parts, sa.workspace), fn);
     const hipError_t e = dtype == XDIT_BF16 ? xdit::launch_attn_bf16(p, g_stream)
                                             : xdit::launch_attn_f32(p, g_stream);
     return hip_status(e, fn);
@@ -424,10 +459,12 @@ int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len,
     if (check_dtype_dim(dtype, head_dim) != XDIT_OK) return -1;
     if (check_dims("xdit_split_workspace_bytes", batch, q_len, kv_len, heads) != XDIT_OK) return -1;
     if (splits > XDIT_MAX_SPLITS) return -1;
-    int s = splits;
-    if (dtype != XDIT_BF16) s = 1;
-    if (s <= 0) s = pick_splits((q_len + kSplitRows - 1) / kSplitRows * batch * heads, (kv_len + 127) / 128);
-    return s > 1 ? split_ws_bytes(batch, q_len, heads, head_dim, esize_of(dtype), s) : 0;
+    const int64_t pairs = part_pairs(batch, q_len, heads);
+    if (dtype != XDIT_BF16 || pairs == 0) return 0;
+    Partition pt;
+    if (splits > 1) pt.parts = pairs * splits;
+    else if (splits <= 0) pt = pick_parts(pairs, kv_len, head_dim);
+    return part_ws_bytes(pt, pairs, head_dim);
 }
 
 int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out, float* lse,

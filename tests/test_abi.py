@@ -150,19 +150,27 @@ def test_ranges_rejections(ranges, q_len, fk, out, lse, code):
 
 
 def test_split_workspace_bytes():
+    """Partitioned launches keep one float32 partial slot (128 query rows x
+    (d + 1)) per cut range, two when ranges may cross query tiles."""
     lib = _lib.lib()
-    # sd3 patch step: 512 queries, 4429 keys, 2 x 24 heads of 64
-    o = 4 * 2 * 512 * 24 * 64 * 2
-    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 4) == o + 4 * 2 * 24 * 512 * 4
+    slot = lambda d: 128 * (d + 1) * 4
+    # sd3 patch step: 512 queries, 4429 keys, 2 x 24 heads of 64: 192 query
+    # tiles, each cut in 4 -> 768 workgroups, one slot each
+    assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 4) == 768 * slot(64)
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 1) == 0
-    # by choice: 192 query tiles keep one round either way -> no split; a
-    # decode-like call (1 x 8 query tiles over 256 key tiles) takes 16
+    # by choice: 192 query tiles keep one round either way -> no partition; a
+    # decode-like call (1 x 8 query tiles over 256 key tiles) cuts each
+    # sweep in 16
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 0) == 0
-    o16 = 16 * 64 * 8 * 128 * 2
-    assert lib.xdit_split_workspace_bytes(1, 64, 32768, 8, 128, 0, 0) == o16 + 16 * 8 * 64 * 4
+    assert lib.xdit_split_workspace_bytes(1, 64, 32768, 8, 128, 0, 0) == 128 * slot(128)
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 1, 4) == 0  # float32: unsplit
-    # a launch that already fills the CUs (pixart patch: 256 query tiles) is not split
+    # a launch that already fills the CUs (pixart patch: 256 query tiles) is not cut
     assert lib.xdit_split_workspace_bytes(2, 1024, 4096, 16, 72, 0, 0) == 0
+    # flux SP share (4224 queries over a 4224-key chunk, 24 heads of 128): 792
+    # query tiles leave the fourth round of 256 CUs nearly empty -> three
+    # rounds of whole sweeps, the 24 left over cut in 10 parts each, one
+    # slot per part
+    assert lib.xdit_split_workspace_bytes(1, 4224, 4224, 24, 128, 0, 0) == 240 * slot(128)
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 17) == -1
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 80, 0, 2) == -1
 

@@ -528,6 +528,71 @@ def test_patch_split(orc, torch, splits):
     assert np.array_equal(to_np(kv), kv_ref), "split patch: buffer not bit-exact"
 
 
+# Balanced partition: the whole launch cut into one contiguous range of
+# (query tile, K/V tile) units per CU (256 ranges), so ranges cross query
+# tiles and a sweep is cut among several workgroups whose partials the fix-up
+# merges.  Query-tile counts do not divide 256.
+BALANCED_CASES = [
+    # B, Nq, Nk, H, d
+    (2, 640, 1600, 3, 64),    # 30 query tiles x 13 K/V tiles: ranges of 1-2 tiles
+    (1, 500, 700, 9, 128),    # ragged last query tile; 11 tiles of 64 keys
+    (2, 700, 1000, 3, 72),    # 36 query tiles x 8 tiles, ragged queries and keys
+    (1, 1100, 3000, 4, 64),   # 36 query tiles x 24 tiles: ranges of 3-4 tiles
+]
+
+
+def _slot_bytes(d):
+    return 128 * (d + 1) * 4
+
+
+@pytest.mark.parametrize("B,Nq,Nk,H,d", BALANCED_CASES)
+def test_chunk_balanced(orc, torch, monkeypatch, B, Nq, Nk, H, d):
+    monkeypatch.setenv("XDIT_PARTITION", "balanced")
+    seed = 430 + Nq + d
+    q = random_io((B, Nq, H, d), "bf16", seed)
+    k = random_io((B, Nk, H, d), "bf16", seed + 1)
+    v = random_io((B, Nk, H, d), "bf16", seed + 2)
+    qg = to_gpu(q, "bf16")
+    need = xd.split_workspace_bytes(qg, Nk, 0)
+    assert need == 2 * 256 * _slot_bytes(d), "the balanced partition was not taken"
+    ws = _workspace(torch, need)
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_chunk_attn_split(qg, to_gpu(k, "bf16"), to_gpu(v, "bf16"), out, lse, 0, ws)
+    torch.cuda.synchronize()
+    ref_o, ref_l = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, "bf16", "balanced out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", "balanced lse")
+
+
+def test_patch_balanced(orc, torch, monkeypatch):
+    """Balanced partition of a ranged patch step: the workgroups' unit
+    shares together store every fresh row once, bit for bit."""
+    monkeypatch.setenv("XDIT_PARTITION", "balanced")
+    B, N, H, d = 2, 1500, 3, 72
+    ranges = [(0, 300), (1400, 100)]
+    q = random_io((B, N, H, d), "bf16", 440)
+    kf = random_io((B, N, H, d), "bf16", 441)
+    vf = random_io((B, N, H, d), "bf16", 442)
+    kv_ref = np.ascontiguousarray(np.stack([random_io((B, N, H, d), "bf16", 443),
+                                            random_io((B, N, H, d), "bf16", 444)]))
+    kv = to_gpu(kv_ref, "bf16")
+    rows = _range_rows(ranges)
+    qs, fks, fvs = q[:, rows].copy(), kf[:, rows].copy(), vf[:, rows].copy()
+    ref_o, ref_l = orc.patch_ranges(qs, kv_ref, ranges, fks, fvs)
+    qg = to_gpu(qs, "bf16")
+    need = xd.split_workspace_bytes(qg, N, 0)
+    assert need == 2 * 256 * _slot_bytes(d), "the balanced partition was not taken"
+    ws = _workspace(torch, need)
+    out = _empty_out(torch, B, len(rows), H, d, "bf16")
+    lse = _lse_buf(torch, B, H, len(rows))
+    xd.xdit_patch_attn_split(qg, kv, ranges, to_gpu(fks, "bf16"), to_gpu(fvs, "bf16"), out, lse, 0, ws)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, "bf16", "balanced patch out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", "balanced patch lse")
+    assert np.array_equal(to_np(kv), kv_ref), "balanced patch: buffer not bit-exact"
+
+
 def test_split_float32_runs_unsplit(orc, torch):
     B, Nq, Nk, H, d = 1, 100, 500, 2, 64
     q = random_io((B, Nq, H, d), "f32", 420)
