@@ -35,17 +35,19 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
-# HBM traffic per launch of the dominant kernel, in bytes: rocprofv3 --pmc
+# HBM traffic per call of the dominant kernel, in bytes: rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE (KiB per dispatch, one counter per run), scaled by
 # what the same counters read for kv_update_kernel copying a known size
 # (FETCH x about 1.995, WRITE x 1.0).  Each entry holds the sha256 prefix of the
 # kernel source it was taken on; a different source reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (50079 + 17969) * 1024, "src": "6c73b0e0cb1a65a1"},
-    ("sd3", "patch_attn"): {"bytes": (59043 + 9216) * 1024, "src": "6c73b0e0cb1a65a1"},
-    ("flux", "chunk_attn"): {"bytes": (115847 + 25746) * 1024, "src": "6c73b0e0cb1a65a1"},
-    ("flux_ring", "chunk_attn"): {"bytes": (135471 + 25771) * 1024, "src": "6c73b0e0cb1a65a1"},
-    ("cog", "chunk_attn"): {"bytes": (133433 + 109989) * 1024, "src": "6c73b0e0cb1a65a1"},
+    ("pixart", "patch_attn"): {"bytes": (49259 + 13865) * 1024, "src": "d2ff18072b4145d1"},
+    ("sd3", "patch_attn"): {"bytes": (59042 + 9216) * 1024, "src": "d2ff18072b4145d1"},
+    # the partitioned sweep and its fix-up, one launch of each per call
+    ("flux", "chunk_attn"): {"bytes": (154618 + 41222) * 1024, "src": "d2ff18072b4145d1"},
+    ("flux_ring", "chunk_attn"): {"bytes": (135475 + 25758) * 1024, "src": "d2ff18072b4145d1"},
+    ("cog", "patch_attn"): {"bytes": (265372 + 19744) * 1024, "src": "d2ff18072b4145d1"},
+    ("cog", "chunk_attn"): {"bytes": (133389 + 109989) * 1024, "src": "d2ff18072b4145d1"},
 }
 
 

@@ -283,7 +283,9 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     // rather than kept live across segments (which made the sweep spill).
     int tid = threadIdx.x;
     if constexpr (PARTS) asm volatile("" : "+v"(tid));
-    const int lane = tid & 63, wave = tid >> 6;
+    // the wave index is uniform: held in a scalar register, so that the LDS
+    // destinations of the tile loads (which go through M0) are scalar too
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 31, hf = lane >> 5;
     const int qb = wave % QB, kh = wave / QB;  // query block, key split
 
