@@ -37,7 +37,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // One lane merges one 16-byte chunk of one output row: 8 bf16 or 4 float
 // elements.  Weights w_r = exp(lse_r - M) / sum_r' exp(lse_r' - M), which
-// equals exp(lse_r - L) with L the merged log-sum-exp.
+// equals exp(lse_r - L) with L the merged log-sum-exp.  The partials' loads
+// of a lane are issued in groups of kGroup before any is used: with one load
+// in flight per lane the merge ran at about half the HBM rate, bound by
+// memory latency.
+constexpr int kGroup = 8;
+
 template <bool BF16>
 __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
     const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -50,6 +55,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
     const int64_t b = bi / a.Nq;
     const int64_t lidx = (b * a.H + h) * a.Nq + i;
     constexpr float kLog2e = 1.4426950408889634f;
+    const int64_t off = row * a.chunks + cc;  // in 16-byte units
 
     float M = -INFINITY;
     for (int r = 0; r < a.n; ++r) M = fmaxf(M, a.lses[r][lidx]);
@@ -66,20 +72,30 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
         for (int r = 0; r < a.n; ++r) sum += exp2f((a.lses[r][lidx] - M) * kLog2e);
         const float inv = 1.f / sum;
         L = M + logf(sum);
-        const int64_t off = row * a.chunks + cc;  // in 16-byte units
-        for (int r = 0; r < a.n; ++r) {
-            const float w = exp2f((a.lses[r][lidx] - M) * kLog2e) * inv;
-            const u32x4 x = ((const u32x4*)a.outs[r])[off];
-            if constexpr (BF16) {
+        for (int r0 = 0; r0 < a.n; r0 += kGroup) {
+            u32x4 x[kGroup];
+            float w[kGroup];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc[2 * e] = __builtin_fmaf(w, bf16lo(x[e]), acc[2 * e]);
-                    acc[2 * e + 1] = __builtin_fmaf(w, bf16hi(x[e]), acc[2 * e + 1]);
+            for (int j = 0; j < kGroup; ++j)
+                if (r0 + j < a.n) {
+                    x[j] = ((const u32x4*)a.outs[r0 + j])[off];
+                    w[j] = a.lses[r0 + j][lidx];
                 }
-            } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(w, __uint_as_float(x[e]), acc[e]);
-            }
+            for (int j = 0; j < kGroup; ++j)
+                if (r0 + j < a.n) {
+                    const float wj = exp2f((w[j] - M) * kLog2e) * inv;
+                    if constexpr (BF16) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            acc[2 * e] = __builtin_fmaf(wj, bf16lo(x[j][e]), acc[2 * e]);
+                            acc[2 * e + 1] = __builtin_fmaf(wj, bf16hi(x[j][e]), acc[2 * e + 1]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wj, __uint_as_float(x[j][e]), acc[e]);
+                    }
+                }
         }
     }
     u32x4 y;
@@ -90,7 +106,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) y[e] = __float_as_uint(acc[e]);
     }
-    ((u32x4*)a.out)[row * a.chunks + cc] = y;
+    ((u32x4*)a.out)[off] = y;
     if (a.lse_out && cc == 0) a.lse_out[lidx] = L;
 }
 
@@ -127,13 +143,23 @@ struct UpdateArgs {
 };
 
 // blockIdx.y = plane * B + b; the slice of one (plane, batch) is contiguous.
+// A lane copies kUpd vectors per pass, all loads issued before the stores.
+constexpr int kUpd = 4;
+
 __global__ __launch_bounds__(kThreads) void kv_update_kernel(UpdateArgs a) {
     const int plane = blockIdx.y / a.B, b = blockIdx.y % a.B;
     const u32x4* src = (plane ? a.fv : a.fk) + (int64_t)b * a.fbatch_vecs;
     u32x4* dst = a.kv + plane * a.plane_vecs + (int64_t)b * a.batch_vecs + a.off_vecs;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
-    for (int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x; v < a.slice_vecs; v += stride)
-        dst[v] = src[v];
+    for (int64_t v0 = (int64_t)blockIdx.x * kThreads + threadIdx.x; v0 < a.slice_vecs; v0 += kUpd * stride) {
+        u32x4 x[kUpd];
+#pragma unroll
+        for (int u = 0; u < kUpd; ++u)
+            if (v0 + u * stride < a.slice_vecs) x[u] = src[v0 + u * stride];
+#pragma unroll
+        for (int u = 0; u < kUpd; ++u)
+            if (v0 + u * stride < a.slice_vecs) dst[v0 + u * stride] = x[u];
+    }
 }
 
 }  // namespace
@@ -154,7 +180,7 @@ hipError_t launch_kv_update(const UpdateParams& p, hipStream_t s) {
     a.slice_vecs = (int64_t)p.len * row_vecs;
     a.B = p.B;
     if (a.slice_vecs == 0 || p.B == 0) return hipSuccess;
-    int64_t bx = (a.slice_vecs + kThreads * 4 - 1) / (kThreads * 4);  // ~4 vectors per lane
+    int64_t bx = (a.slice_vecs + kThreads * kUpd - 1) / (kThreads * kUpd);  // one pass of kUpd vectors per lane
     if (bx < 1) bx = 1;
     if (bx > 65535) bx = 65535;
     hipLaunchKernelGGL(kv_update_kernel, dim3((unsigned)bx, (unsigned)(2 * p.B)), dim3(kThreads), 0, s, a);

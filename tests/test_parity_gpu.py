@@ -157,6 +157,30 @@ def test_chunks_then_merge_equal_full(orc, torch, tile_shape, dtype, d):
     check_lse(to_np(lse), ml, dtype, "merge lse vs oracle merge")
 
 
+@pytest.mark.parametrize("n", [9, 17, 64])
+def test_merge_many_partials(orc, torch, n):
+    """n above one group of in-flight loads (8), ragged, up to the most one
+    call accepts; a third of the partials empty."""
+    B, Nq, H, d = 1, 45, 3, 72
+    outs, lses, outs_np, lses_np = [], [], [], []
+    for r in range(n):
+        o = random_io((B, Nq, H, d), "bf16", 600 + r)
+        l = (random_io((B, H, Nq), "f32", 700 + r) * 3).astype(np.float32)
+        if r % 3 == 1:
+            l[:] = -np.inf
+        outs_np.append(o)
+        lses_np.append(l)
+        outs.append(to_gpu(o, "bf16"))
+        lses.append(torch.from_numpy(l).cuda())
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_lse_merge(outs, lses, n, out, lse)
+    torch.cuda.synchronize()
+    mo, ml = orc.merge(outs_np, lses_np)
+    check_out(to_np(out), mo, "bf16", f"merge of {n}")
+    check_lse(to_np(lse), ml, "bf16", f"merge lse of {n}")
+
+
 def test_merge_single_partial_is_copy(torch):
     B, Nq, H, d = 1, 77, 3, 72
     o = to_gpu(random_io((B, Nq, H, d), "bf16", 30), "bf16")
