@@ -542,15 +542,31 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
             const int kb = ks >> 1, i0 = 8 * (ks & 1);
+            // row sums where no padding row of V^T produces them: at d = 64 as
+            // float32 adds of the weights, at d = 128 of the bf16 weights, one
+            // v_dot2 with ones per pair (fewer VALU instructions; measured
+            // 2 % faster at d = 128, 1-3 % slower in the d = 64 patch step)
+            constexpr bool SUM_F32 = !C::SUM_BY_MFMA && D <= 96, SUM_DOT = !C::SUM_BY_MFMA && D > 96;
             float p[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][i0 + e], a.c2, -mc));
-                if constexpr (!C::SUM_BY_MFMA) l_run += p[e];
+                if constexpr (SUM_F32) l_run += p[e];
             }
+            typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+            typedef float f32x2_t __attribute__((ext_vector_type(2)));
+            const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
             u32x4 pw;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) pw[w] = pack_bf16x2(p[2 * w], p[2 * w + 1]);
+            for (int w = 0; w < 4; ++w) {
+                // one v_cvt_pk_bf16_f32 per pair (round to nearest even)
+                const bf16x2_t pp = __builtin_convertvector((f32x2_t{p[2 * w], p[2 * w + 1]}), bf16x2_t);
+                pw[w] = __builtin_bit_cast(uint32_t, pp);
+                // the pair goes to the dot product as the converted value:
+                // passed as a bit cast of an element of pw, every dot product
+                // read pw's first element (a miscompile of this toolchain)
+                if constexpr (SUM_DOT) l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run, false);
+            }
             pb[ks] = __builtin_bit_cast(bf16x8, pw);
         }
     };
