@@ -589,6 +589,28 @@ def test_chunk_balanced(orc, torch, monkeypatch, B, Nq, Nk, H, d):
     check_lse(lse.cpu().numpy(), ref_l, "bf16", "balanced lse")
 
 
+def test_chunk_whole_rounds_then_cut(orc, torch, monkeypatch):
+    """The library's own partition for 272 query tiles (one full round of
+    256 CUs and 16 left over): the first 256 sweep whole, each of the 16
+    left over is cut into 16 parts, one slot per part."""
+    monkeypatch.delenv("XDIT_PARTITION", raising=False)
+    B, Nq, Nk, H, d = 1, 2048, 4096, 17, 64
+    q = random_io((B, Nq, H, d), "bf16", 450)
+    k = random_io((B, Nk, H, d), "bf16", 451)
+    v = random_io((B, Nk, H, d), "bf16", 452)
+    qg = to_gpu(q, "bf16")
+    need = xd.split_workspace_bytes(qg, Nk, 0)
+    assert need == 16 * 16 * _slot_bytes(d), "the whole-rounds-then-cut partition was not taken"
+    ws = _workspace(torch, need)
+    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_chunk_attn_split(qg, to_gpu(k, "bf16"), to_gpu(v, "bf16"), out, lse, 0, ws)
+    torch.cuda.synchronize()
+    ref_o, ref_l = orc.attention(q, k, v)
+    check_out(to_np(out), ref_o, "bf16", "whole + cut out")
+    check_lse(lse.cpu().numpy(), ref_l, "bf16", "whole + cut lse")
+
+
 def test_patch_balanced(orc, torch, monkeypatch):
     """Balanced partition of a ranged patch step: the workgroups' unit
     shares together store every fresh row once, bit for bit."""
