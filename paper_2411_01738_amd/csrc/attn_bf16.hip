@@ -210,7 +210,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // Transposing LDS read (ds_read_b64_tr_b16) at byte address a + OFF, issued
-// without a wait: the caller waits with lds_wait() before using the result.
+// without a wait: the caller waits with lds_wait_upto() before using the result.
 // Written as inline assembly so that the compiler does not also drain the
 // in-flight tile loads before it (it cannot tell that they target other LDS
 // bytes).
@@ -221,23 +221,15 @@ __device__ __forceinline__ u32x2 tr_read(uint32_t a) {
     asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
     return r;
 }
-// Wait for all LDS reads of this wave; the operands are the registers those
-// reads fill, so nothing reads them before the wait.
-template <int NS, int NB>
-__device__ __forceinline__ void lds_wait_all(u32x2 (&r)[NS][NB][2]) {
-    asm volatile("s_waitcnt lgkmcnt(0)");
-#pragma unroll
-    for (int i = 0; i < NS; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(r[i][j][0]), "+v"(r[i][j][1]));
+// Wait until at most N LDS reads of this wave are in flight (they complete
+// in issue order), then mark the registers of the reads that were covered.
+__device__ __forceinline__ void lds_hold_one(u32x2& r) { asm volatile("" : "+v"(r)); }
+template <int N, typename... R>
+__device__ __forceinline__ void lds_wait_upto(R&... r) {
+    static_assert(N >= 0, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N < 15 ? N : 15));
+    (lds_hold_one(r), ...);
 }
-// Registers filled by LDS reads that an earlier lds_wait_all has covered.
-template <int NT>
-__device__ __forceinline__ void lds_hold(u32x2 (&r)[NT][2]) {
-#pragma unroll
-    for (int i = 0; i < NT; ++i) asm volatile("" : "+v"(r[i][0]), "+v"(r[i][1]));
-}
-
 // Key of S^T row x (0..31) of a 32-key block: x = 16a + 8e + 4h + j is key
 // 16a + 4j + 2e + h when PERM, key x otherwise.
 template <bool PERM>
@@ -571,21 +563,22 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         }
     };
     // V^T operands of tile t, all NKS k-steps, issued without a wait: the
-    // full blocks in vr, the tail (one operand per pair of k-steps) in vt
+    // full blocks in vr, the tail (one operand per pair of k-steps) in vt.
+    // They are issued in the order pv consumes them: per k-step its full
+    // blocks, then after each odd step the tail operand of the pair.
     constexpr int NPT = C::TAIL ? NKS / 2 : 0;
+    // reads of k-step j; reads issued after those of step ks's full blocks
+    // (tail = false) or after its tail operand (tail = true)
+    constexpr auto vt_reads = [](int j) { return 2 * C::DBLK + (C::TAIL && (j & 1) ? 2 : 0); };
+    constexpr auto vt_after = [vt_reads](int ks, bool tail) {
+        int n = 0;
+        for (int j = ks + 1; j < NKS; ++j) n += vt_reads(j);
+        return n + (!tail && C::TAIL && (ks & 1) ? 2 : 0);
+    };
     auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2], u32x2 (&vt)[NPT > 0 ? NPT : 1][2]) {
         const uint32_t vst = lds_u32 + (uint32_t)((t % NST) * C::STAGE_BYTES);
-        if constexpr (C::TAIL) {
-            // lanes of padding dims keep reading the constant chunk
-            const bool cst = vtaddr >= (uint32_t)C::CONST_OFF;
-#pragma unroll
-            for (int pp = 0; pp < NPT; ++pp) {
-                const uint32_t a0 = vst + vtaddr + (cst ? 0u : (uint32_t)(32 * pp * C::ROWB));
-                const uint32_t a1 = vst + vtaddr + (cst ? 0u : (uint32_t)((32 * pp + C::E_ROWS) * C::ROWB));
-                vt[pp][0] = tr_read<0>(a0);
-                vt[pp][1] = tr_read<0>(a1);
-            }
-        }
+        // lanes of padding dims keep reading the constant chunk
+        const bool cst = vtaddr >= (uint32_t)C::CONST_OFF;
         static_for<0, NKS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
             static_for<0, C::DBLK>([&](auto dbc) {
@@ -598,6 +591,13 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
                     vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB>(vst + vaddr[db][0]);
                 }
             });
+            if constexpr (C::TAIL && (ks & 1)) {
+                constexpr int pp = ks >> 1;
+                const uint32_t a0 = vst + vtaddr + (cst ? 0u : (uint32_t)(32 * pp * C::ROWB));
+                const uint32_t a1 = vst + vtaddr + (cst ? 0u : (uint32_t)((32 * pp + C::E_ROWS) * C::ROWB));
+                vt[pp][0] = tr_read<0>(a0);
+                vt[pp][1] = tr_read<0>(a1);
+            }
         });
     };
     // O^T += V^T P^T over the NKS k-steps.  Tail: for each pair of k-steps,
@@ -605,36 +605,44 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     // operands of queries 0..15 ({x.r0, y.r0, x.r2, y.r2}: rows of 16 lanes)
     // and 16..31 ({x.r1, y.r1, x.r3, y.r3}); group g then holds the keys of
     // step 2p + (g & 1), half g >> 1, as the tail V^T operand does.
-    auto pv = [&](const u32x2 (&vr)[NKS][C::DBLK][2], const u32x2 (&vt)[NPT > 0 ? NPT : 1][2],
-                  const bf16x8 (&pb)[NKS]) {
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
+    // The V^T reads of read_vt are still in flight: each k-step waits only
+    // for its own operands, so the first products start while the later
+    // operands arrive.
+    auto pv = [&](u32x2 (&vr)[NKS][C::DBLK][2], u32x2 (&vt)[NPT > 0 ? NPT : 1][2], const bf16x8 (&pb)[NKS]) {
+        static_for<0, NKS>([&](auto ksc) {
+            constexpr int ks = decltype(ksc)::value;
+            if constexpr (C::DBLK == 2)
+                lds_wait_upto<vt_after(ks, false)>(vr[ks][0][0], vr[ks][0][1], vr[ks][1][0], vr[ks][1][1]);
+            else if constexpr (C::DBLK == 4)
+                lds_wait_upto<vt_after(ks, false)>(vr[ks][0][0], vr[ks][0][1], vr[ks][1][0], vr[ks][1][1],
+                                                   vr[ks][2][0], vr[ks][2][1], vr[ks][3][0], vr[ks][3][1]);
+            else
+                static_assert(C::DBLK == 2 || C::DBLK == 4, "full blocks of V^T");
 #pragma unroll
             for (int db = 0; db < C::DBLK; ++db) {
                 const u32x4 v4 = {vr[ks][db][0][0], vr[ks][db][0][1], vr[ks][db][1][0], vr[ks][db][1][1]};
                 oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v4), pb[ks], oacc[db],
                                                                    0, 0, 0);
             }
-            if constexpr (C::TAIL) {
-                if (ks & 1) {
-                    const u32x4 x = __builtin_bit_cast(u32x4, pb[ks - 1]), y = __builtin_bit_cast(u32x4, pb[ks]);
-                    u32x4 b0, b1;
+            if constexpr (C::TAIL && (ks & 1)) {
+                constexpr int pp = ks >> 1;
+                lds_wait_upto<vt_after(ks, true)>(vt[pp][0], vt[pp][1]);
+                const u32x4 x = __builtin_bit_cast(u32x4, pb[ks - 1]), y = __builtin_bit_cast(u32x4, pb[ks]);
+                u32x4 b0, b1;
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
-                        b0[w] = r[0];
-                        b1[w] = r[1];
-                    }
-                    const int pp = ks >> 1;
-                    const u32x4 v4 = {vt[pp][0][0], vt[pp][0][1], vt[pp][1][0], vt[pp][1][1]};
-                    const bf16x8 va = __builtin_bit_cast(bf16x8, v4);
-                    otail[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b0), otail[0],
-                                                                       0, 0, 0);
-                    otail[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b1), otail[1],
-                                                                       0, 0, 0);
+                for (int w = 0; w < 4; ++w) {
+                    const auto r = __builtin_amdgcn_permlane16_swap(x[w], y[w], false, false);
+                    b0[w] = r[0];
+                    b1[w] = r[1];
                 }
+                const u32x4 v4 = {vt[pp][0][0], vt[pp][0][1], vt[pp][1][0], vt[pp][1][1]};
+                const bf16x8 va = __builtin_bit_cast(bf16x8, v4);
+                otail[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b0), otail[0],
+                                                                   0, 0, 0);
+                otail[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8, b1), otail[1],
+                                                                   0, 0, 0);
             }
-        }
+        });
     };
 
     // Wait until at most the loads of the N most recently issued tiles are in
@@ -683,8 +691,6 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
             if constexpr (MASK) mask(t + 1, sn);
             mx = row_max(sn);
         }
-        lds_wait_all(vr);
-        if constexpr (C::TAIL) lds_hold(vt);
         pv(vr, vt, pb);
         if constexpr (NEXT) update_max(mx);
     };
