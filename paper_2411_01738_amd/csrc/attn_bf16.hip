@@ -112,6 +112,7 @@ struct Cfg {
         else return 0;
     }
     static constexpr bool E_SPLIT = CH == 8 || CH == 16;
+    static constexpr bool SWIZZLED = CH == 8 || CH == 16;  // swz is not identically zero
     static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
     static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
@@ -481,9 +482,16 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
-                uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
-                if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
-                const bf16x8 ka = *(const bf16x8*)(st + ad);
+                bf16x8 ka;
+                if (!C::SWIZZLED && 2 * kk + 1 < C::CH) {
+                    // unswizzled rows: chunk 2kk + hf sits 32kk bytes past
+                    // chunk hf, an immediate offset of one address
+                    ka = *(const bf16x8*)(st + kaddr[0] + 32 * kk + 32 * kb * C::ROWB);
+                } else {
+                    uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
+                    if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
+                    ka = *(const bf16x8*)(st + ad);
+                }
                 s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s[kb], 0, 0, 0);
             }
     };
@@ -587,8 +595,10 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
                     vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
                     vr[ks][db][1] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][NE - 1]);
                 } else {
-                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
-                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB>(vst + vaddr[db][0]);
+                    // unswizzled rows: block db's dims sit 64db bytes past block 0's
+                    static_assert(!C::SWIZZLED, "one address for all blocks");
+                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB + 64 * db>(vst + vaddr[0][0]);
+                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB + 64 * db>(vst + vaddr[0][0]);
                 }
             });
             if constexpr (C::TAIL && (ks & 1)) {

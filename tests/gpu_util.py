@@ -37,7 +37,9 @@ def to_np(t) -> np.ndarray:
     return t.float().cpu().numpy()
 
 
-def check_out(gpu, ref, dtype: str, what: str):
+def check_out(gpu, ref, dtype: str, what: str, scale: float = 1.0):
+    """Element-wise check against the stated bars; `scale` (>= 1) widens
+    both for inputs whose conditioning the caller has bounded."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert gpu.shape == ref.shape, f"{what}: shape {gpu.shape} vs {ref.shape}"
@@ -45,10 +47,10 @@ def check_out(gpu, ref, dtype: str, what: str):
     if gpu.size == 0:
         return
     err = np.abs(gpu - ref)
-    t = TOL[dtype]
+    t = {k: v * max(1.0, scale) for k, v in TOL[dtype].items()}
     rms = float(np.sqrt(np.mean(err ** 2)))
-    assert err.max() <= t["max_abs"], f"{what}: max abs err {err.max():.3e} > {t['max_abs']}"
-    assert rms <= t["rms"], f"{what}: rms err {rms:.3e} > {t['rms']}"
+    assert err.max() <= t["max_abs"], f"{what}: max abs err {err.max():.3e} > {t['max_abs']:.3e}"
+    assert rms <= t["rms"], f"{what}: rms err {rms:.3e} > {t['rms']:.3e}"
 
 
 def check_lse(gpu, ref, dtype: str, what: str):

@@ -125,6 +125,84 @@ def test_constant_values_give_constant_output(torch, d):
     assert np.all(err <= 2 * 2.0 ** -9 * np.abs(c) * 1.01 + 1e-7), err.max()
 
 
+def _extreme_inputs(kind: str, dtype: str, B: int, Nq: int, Nk: int, H: int, d: int, seed: int):
+    """Score distributions that drive the online softmax's reference max:
+    "peaked": q, k ~ N(0, 6^2), scores spread over hundreds of log2 units, so
+      nearly one-hot rows and rescales in the first tiles;
+    "rising": every query along one direction u and key j = (j / Nk) 30 u +
+      noise, so each row's max grows along the whole sweep (a rescale in
+      most tiles, early weights underflowing to zero);
+    "negative": keys pointing against the queries, every score near -300
+      (nats), so the reference sits far below zero throughout."""
+    from paper_2411_01738_amd.inputs import to_io
+
+    rng = np.random.Generator(np.random.PCG64(seed))
+    v = random_io((B, Nk, H, d), dtype, seed + 1)
+    if kind == "peaked":
+        return random_io((B, Nq, H, d), dtype, seed + 2, 6.0), random_io((B, Nk, H, d), dtype, seed + 3, 6.0), v
+    u = rng.standard_normal((1, 1, H, d)).astype(np.float32)
+    u /= np.linalg.norm(u, axis=-1, keepdims=True)
+    q = u * np.float32(3.0 * np.sqrt(d)) + 0.3 * rng.standard_normal((B, Nq, H, d)).astype(np.float32)
+    noise = 0.3 * rng.standard_normal((B, Nk, H, d)).astype(np.float32)
+    if kind == "rising":
+        k = (np.arange(Nk, dtype=np.float32) / Nk * 30.0)[None, :, None, None] * u + noise
+    else:
+        k = -100.0 * u + noise
+    return to_io(q, dtype), to_io(k.astype(np.float32), dtype), v
+
+
+def _f32_score_scale(q, k, v) -> float:
+    """Float32 I/O: a score s carries a rounding error of about
+    sqrt(d) |s| 2^-24 from its float32 dot product, and the output moves by at
+    most 2 max|v| times the score error; returns that bound over the stated
+    1e-5 bar (at least 1).  It matters only when scores reach hundreds."""
+    d = q.shape[-1]
+    s = np.einsum("bihc,bjhc->bhij", q.astype(np.float64), k.astype(np.float64)) / np.sqrt(d)
+    bound = 2.0 * np.abs(v).max() * np.sqrt(d) * np.abs(s).max() * 2.0 ** -24
+    return max(1.0, bound / 1e-5)
+
+
+@pytest.mark.parametrize("kind", ["peaked", "rising", "negative"])
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 72), ("bf16", 128), ("f32", 72)])
+def test_chunk_softmax_extremes(orc, torch, tile_shape, kind, dtype, d):
+    """Online softmax against the oracle where scores are far from N(0, 1):
+    the reference max is raised often, late, or sits far below zero."""
+    B, Nq, Nk, H = 1, 140, 1100, 2
+    q, k, v = _extreme_inputs(kind, dtype, B, Nq, Nk, H, d, 500 + d)
+    ref_o, ref_l = orc.attention(q, k, v)
+    out = _empty_out(torch, B, Nq, H, d, dtype)
+    lse = _lse_buf(torch, B, H, Nq)
+    xd.xdit_chunk_attn(to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype), out, lse)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, dtype, f"{kind} out", _f32_score_scale(q, k, v) if dtype == "f32" else 1.0)
+    check_lse(to_np(lse), ref_l, dtype, f"{kind} lse")
+
+
+@pytest.mark.parametrize("kind", ["peaked", "rising"])
+def test_patch_softmax_extremes(orc, torch, kind):
+    """The patch step on the same distributions (fresh rows in the middle of
+    the sweep, buffer rows around them)."""
+    B, N, H, d, off, ln = 1, 1100, 2, 72, 400, 300
+    q_all, k, v = _extreme_inputs(kind, "bf16", B, N, N, H, d, 900)
+    stale_k = random_io((B, N, H, d), "bf16", 901)
+    stale_v = random_io((B, N, H, d), "bf16", 902)
+    kv = np.ascontiguousarray(np.stack([stale_k, stale_v]))
+    kv[0][:, :off] = k[:, :off]
+    kv[0][:, off + ln:] = k[:, off + ln:]
+    kv[1][:, :off] = v[:, :off]
+    kv[1][:, off + ln:] = v[:, off + ln:]
+    q = q_all[:, off:off + ln].copy()
+    fk, fv = k[:, off:off + ln].copy(), v[:, off:off + ln].copy()
+    ref_o, _ = orc.patch(q, kv.copy(), off, fk, fv)
+    kv_g = to_gpu(kv, "bf16")
+    out = _empty_out(torch, B, ln, H, d, "bf16")
+    xd.xdit_patch_attn(to_gpu(q, "bf16"), kv_g, off, ln, to_gpu(fk, "bf16"), to_gpu(fv, "bf16"), out)
+    torch.cuda.synchronize()
+    check_out(to_np(out), ref_o, "bf16", f"{kind} patch out")
+    assert np.array_equal(to_np(kv_g), np.concatenate([k[None], v[None]]).astype(np.float32)), \
+        "buffer after the step differs from the fresh K/V"
+
+
 # ---------------------------------------------------------------------------
 # LSE merge
 # ---------------------------------------------------------------------------
