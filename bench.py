@@ -41,13 +41,13 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # (FETCH x about 1.995, WRITE x 1.0).  Each entry holds the sha256 prefix of the
 # kernel source it was taken on; a different source reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (49128 + 13869) * 1024, "src": "ed72d6657cc278e8"},
-    ("sd3", "patch_attn"): {"bytes": (59014 + 9216) * 1024, "src": "ed72d6657cc278e8"},
+    ("pixart", "patch_attn"): {"bytes": (49222 + 13866) * 1024, "src": "d1fa622b5a125fcf"},
+    ("sd3", "patch_attn"): {"bytes": (58969 + 9216) * 1024, "src": "d1fa622b5a125fcf"},
     # the partitioned sweep and its fix-up, one launch of each per call
-    ("flux", "chunk_attn"): {"bytes": (154438 + 41221) * 1024, "src": "ed72d6657cc278e8"},
-    ("flux_ring", "chunk_attn"): {"bytes": (135229 + 25767) * 1024, "src": "ed72d6657cc278e8"},
-    ("cog", "patch_attn"): {"bytes": (265175 + 19744) * 1024, "src": "ed72d6657cc278e8"},
-    ("cog", "chunk_attn"): {"bytes": (133353 + 109989) * 1024, "src": "ed72d6657cc278e8"},
+    ("flux", "chunk_attn"): {"bytes": (154455 + 41222) * 1024, "src": "d1fa622b5a125fcf"},
+    ("flux_ring", "chunk_attn"): {"bytes": (135408 + 25762) * 1024, "src": "d1fa622b5a125fcf"},
+    ("cog", "patch_attn"): {"bytes": (265119 + 19744) * 1024, "src": "d1fa622b5a125fcf"},
+    ("cog", "chunk_attn"): {"bytes": (133311 + 109989) * 1024, "src": "d1fa622b5a125fcf"},
 }
 
 
