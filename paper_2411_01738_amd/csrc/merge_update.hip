@@ -43,7 +43,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // memory latency.
 constexpr int kGroup = 8;
 
-template <bool BF16>
+// NP > 0: exactly NP partials, known at compile time: every load of a lane
+// (its NP LSEs and NP chunks) is issued before any is used, one memory round
+// trip per lane.  NP = 0: any n, the partials in groups of kGroup.
+template <bool BF16, int NP>
 __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
     const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (g >= a.total) return;
@@ -56,46 +59,84 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs a) {
     const int64_t lidx = (b * a.H + h) * a.Nq + i;
     constexpr float kLog2e = 1.4426950408889634f;
     const int64_t off = row * a.chunks + cc;  // in 16-byte units
-
-    float M = -INFINITY;
-    for (int r = 0; r < a.n; ++r) M = fmaxf(M, a.lses[r][lidx]);
-
     constexpr int EPC = BF16 ? 8 : 4;
     float acc[EPC];
 #pragma unroll
     for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
     float L = -INFINITY;
-    if (M != -INFINITY) {
-        // (lse_r - M) is exactly 0 for the largest partial, so its weight is
-        // exactly 1 before normalisation and n = 1 reproduces the partial.
-        float sum = 0.f;
-        for (int r = 0; r < a.n; ++r) sum += exp2f((a.lses[r][lidx] - M) * kLog2e);
-        const float inv = 1.f / sum;
-        L = M + logf(sum);
-        for (int r0 = 0; r0 < a.n; r0 += kGroup) {
-            u32x4 x[kGroup];
-            float w[kGroup];
+
+    if constexpr (NP > 0) {
+        u32x4 x[NP];
+        float l[NP];
 #pragma unroll
-            for (int j = 0; j < kGroup; ++j)
-                if (r0 + j < a.n) {
-                    x[j] = ((const u32x4*)a.outs[r0 + j])[off];
-                    w[j] = a.lses[r0 + j][lidx];
-                }
+        for (int r = 0; r < NP; ++r) {
+            l[r] = a.lses[r][lidx];
+            x[r] = ((const u32x4*)a.outs[r])[off];
+        }
+        float M = l[0];
 #pragma unroll
-            for (int j = 0; j < kGroup; ++j)
-                if (r0 + j < a.n) {
-                    const float wj = exp2f((w[j] - M) * kLog2e) * inv;
-                    if constexpr (BF16) {
+        for (int r = 1; r < NP; ++r) M = fmaxf(M, l[r]);
+        if (M != -INFINITY) {
+            // (lse_r - M) is exactly 0 for the largest partial, so its weight
+            // is exactly 1 before normalisation and n = 1 reproduces the partial
+            float w[NP], sum = 0.f;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            acc[2 * e] = __builtin_fmaf(wj, bf16lo(x[j][e]), acc[2 * e]);
-                            acc[2 * e + 1] = __builtin_fmaf(wj, bf16hi(x[j][e]), acc[2 * e + 1]);
-                        }
-                    } else {
+            for (int r = 0; r < NP; ++r) {
+                w[r] = exp2f((l[r] - M) * kLog2e);
+                sum += w[r];
+            }
+            const float inv = 1.f / sum;
+            L = M + logf(sum);
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wj, __uint_as_float(x[j][e]), acc[e]);
+            for (int r = 0; r < NP; ++r) {
+                const float wr = w[r] * inv;
+                if constexpr (BF16) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc[2 * e] = __builtin_fmaf(wr, bf16lo(x[r][e]), acc[2 * e]);
+                        acc[2 * e + 1] = __builtin_fmaf(wr, bf16hi(x[r][e]), acc[2 * e + 1]);
                     }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wr, __uint_as_float(x[r][e]), acc[e]);
                 }
+            }
+        }
+    } else {
+        float M = -INFINITY;
+        for (int r = 0; r < a.n; ++r) M = fmaxf(M, a.lses[r][lidx]);
+        if (M != -INFINITY) {
+            // (lse_r - M) is exactly 0 for the largest partial, so its weight is
+            // exactly 1 before normalisation and n = 1 reproduces the partial.
+            float sum = 0.f;
+            for (int r = 0; r < a.n; ++r) sum += exp2f((a.lses[r][lidx] - M) * kLog2e);
+            const float inv = 1.f / sum;
+            L = M + logf(sum);
+            for (int r0 = 0; r0 < a.n; r0 += kGroup) {
+                u32x4 x[kGroup];
+                float w[kGroup];
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j)
+                    if (r0 + j < a.n) {
+                        x[j] = ((const u32x4*)a.outs[r0 + j])[off];
+                        w[j] = a.lses[r0 + j][lidx];
+                    }
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j)
+                    if (r0 + j < a.n) {
+                        const float wj = exp2f((w[j] - M) * kLog2e) * inv;
+                        if constexpr (BF16) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                acc[2 * e] = __builtin_fmaf(wj, bf16lo(x[j][e]), acc[2 * e]);
+                                acc[2 * e + 1] = __builtin_fmaf(wj, bf16hi(x[j][e]), acc[2 * e + 1]);
+                            }
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wj, __uint_as_float(x[j][e]), acc[e]);
+                        }
+                    }
+            }
         }
     }
     u32x4 y;
@@ -126,7 +167,16 @@ hipError_t launch_merge(const MergeParams& p, hipStream_t s) {
     a.total = (int64_t)p.B * p.Nq * p.H * a.chunks;
     if (a.total == 0) return hipSuccess;
     const int64_t blocks = (a.total + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL((merge_kernel<BF16>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    const dim3 grid((unsigned)blocks), block(kThreads);
+    switch (p.n) {
+        case 1: hipLaunchKernelGGL((merge_kernel<BF16, 1>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((merge_kernel<BF16, 2>), grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL((merge_kernel<BF16, 3>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((merge_kernel<BF16, 4>), grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL((merge_kernel<BF16, 6>), grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL((merge_kernel<BF16, 8>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((merge_kernel<BF16, 0>), grid, block, 0, s, a); break;
+    }
     return hipGetLastError();
 }
 

@@ -235,10 +235,11 @@ def test_chunks_then_merge_equal_full(orc, torch, tile_shape, dtype, d):
     check_lse(to_np(lse), ml, dtype, "merge lse vs oracle merge")
 
 
-@pytest.mark.parametrize("n", [9, 17, 64])
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 8, 9, 17, 64])
 def test_merge_many_partials(orc, torch, n):
-    """n above one group of in-flight loads (8), ragged, up to the most one
-    call accepts; a third of the partials empty."""
+    """Every partial count the library compiles a form for (2, 3, 4, 6, 8),
+    counts that take the general form (5; above one group of in-flight loads,
+    9 and 17; the most one call accepts, 64); a third of the partials empty."""
     B, Nq, H, d = 1, 45, 3, 72
     outs, lses, outs_np, lses_np = [], [], [], []
     for r in range(n):
