@@ -318,8 +318,22 @@ def main():
         for rc in rcs:
             _lib.check(rc)
         us = a.elapsed_time(b) * 1e3 / reps
+        # cold: each launch after a 1 GiB write that evicts L2 and the MALL
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        cold = []
+        for _ in range(20):
+            flush.fill_(1.0)
+            a.record(stream)
+            _lib.check(L.xdit_lse_merge(*mrg))
+            b.record(stream)
+            torch.cuda.synchronize()
+            cold.append(a.elapsed_time(b) * 1e3)
+        del flush
+        cold_us = sorted(cold)[len(cold) // 2]
         kern["lse_merge"].update(back_to_back_us=round(us, 3),
-                                 back_to_back_gbs=round(hp.merge_bytes() / us / 1e3, 1))
+                                 back_to_back_gbs=round(hp.merge_bytes() / us / 1e3, 1),
+                                 cold_median_us=round(cold_us, 3),
+                                 cold_gbs=round(hp.merge_bytes() / cold_us / 1e3, 1))
 
     step_flops = hp.step_flops()
     value = step_flops / (ms_per_step / 1e3) / 1e12
