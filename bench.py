@@ -38,29 +38,27 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # HBM traffic per call of the dominant kernel, in bytes: rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE (KiB per dispatch, one counter per run), scaled by
 # what the same counters read for kv_update_kernel copying a known size
-# (FETCH x about 1.995, WRITE x 1.0).  Each entry holds the sha256 prefix of the
-# kernel source it was taken on; a different source reports null.
+# (FETCH x about 1.995, WRITE x 1.0).  Each entry holds the fingerprint of the
+# kernel build it was taken on (sha256 prefix of the source and its compile
+# flags); a different build reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (49222 + 13866) * 1024, "src": "d1fa622b5a125fcf"},
-    ("sd3", "patch_attn"): {"bytes": (58969 + 9216) * 1024, "src": "d1fa622b5a125fcf"},
+    ("pixart", "patch_attn"): {"bytes": (49151 + 13875) * 1024, "src": "0ae64fdbe1062094"},
+    ("sd3", "patch_attn"): {"bytes": (58953 + 9216) * 1024, "src": "0ae64fdbe1062094"},
     # the partitioned sweep and its fix-up, one launch of each per call
-    ("flux", "chunk_attn"): {"bytes": (154455 + 41222) * 1024, "src": "d1fa622b5a125fcf"},
-    ("flux_ring", "chunk_attn"): {"bytes": (135408 + 25762) * 1024, "src": "d1fa622b5a125fcf"},
-    ("cog", "patch_attn"): {"bytes": (265119 + 19744) * 1024, "src": "d1fa622b5a125fcf"},
-    ("cog", "chunk_attn"): {"bytes": (133311 + 109989) * 1024, "src": "d1fa622b5a125fcf"},
+    ("flux", "chunk_attn"): {"bytes": (154455 + 41224) * 1024, "src": "0ae64fdbe1062094"},
+    ("flux_ring", "chunk_attn"): {"bytes": (135360 + 25763) * 1024, "src": "0ae64fdbe1062094"},
+    ("cog", "patch_attn"): {"bytes": (264983 + 19744) * 1024, "src": "0ae64fdbe1062094"},
+    ("cog", "chunk_attn"): {"bytes": (133307 + 109989) * 1024, "src": "0ae64fdbe1062094"},
 }
 
 
 def traffic_of(workload: str, kind: str):
-    import hashlib
+    from paper_2411_01738_amd.build import kernel_fingerprint
 
     e = MEASURED_TRAFFIC.get((workload, kind))
     if e is None:
         return None
-    src = os.path.join(ROOT, "paper_2411_01738_amd", "csrc", "attn_bf16.hip")
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    return e["bytes"] if sha == e["src"] else None
+    return e["bytes"] if kernel_fingerprint() == e["src"] else None
 
 
 def parse():
