@@ -81,7 +81,8 @@ def cpu_baseline(w, t, target_s: float):
     """fp64 oracle on a bounded sample of the workload: whole calls of the step
     in order (patch steps, else chunk steps) until about target_s seconds have
     been spent; when one call alone would take far longer, an evenly spaced
-    subset of its query rows.  Scaled to TFLOP/s of algorithmic work."""
+    subset of its query rows.  Scaled to TFLOP/s of algorithmic work.  The
+    same is then run on one thread for a third of the time."""
     import numpy as np
 
     import oracle
@@ -119,44 +120,57 @@ def cpu_baseline(w, t, target_s: float):
                          lambda rows, k=k, v=v: orc.attention(q, k, v, rows=rows),
                          lambda n, nk=e - s: attn(n, nk)))
 
-    # calibrate the cost of one (query row x key) on a few rows of the first
-    # call; the first probe also starts the oracle's thread pool
-    desc0, nq0, nk0, run0, _ = jobs[0]
-    probe = np.linspace(0, nq0 - 1, min(64, nq0)).astype(np.int64)
-    run0(probe)
-    t0 = time.perf_counter()
-    run0(probe)
-    per_unit = (time.perf_counter() - t0) / (len(probe) * nk0)
-    # whole calls in step order, the step repeated if it is short, the last
-    # call cut to an evenly spaced subset of its rows to stay near target_s
-    flops, spent, parts = 0.0, 0.0, []
-    for rep in range(1000):
-        for desc, nq, nk, run, flops_of in jobs:
-            left = target_s - spent
-            if left <= 0.05 * target_s:
-                break
-            n = min(nq, max(1, int(left / (per_unit * nk))))
-            rows = (np.arange(nq, dtype=np.int64) if n >= nq
-                    else np.linspace(0, nq - 1, n).astype(np.int64))
-            t0 = time.perf_counter()
-            run(rows)
-            dt = time.perf_counter() - t0
-            spent += dt
-            per_unit = dt / (len(rows) * nk)
-            flops += flops_of(len(rows))
-            parts.append(f"{desc} ({len(rows)}/{nq} rows)")
-        else:
-            continue
-        break
+    def sample(budget_s):
+        # calibrate the cost of one (query row x key) on a few rows of the
+        # first call; the first probe also starts the oracle's thread pool
+        desc0, nq0, nk0, run0, _ = jobs[0]
+        probe = np.linspace(0, nq0 - 1, min(64, nq0)).astype(np.int64)
+        run0(probe)
+        t0 = time.perf_counter()
+        run0(probe)
+        per_unit = (time.perf_counter() - t0) / (len(probe) * nk0)
+        # whole calls in step order, the step repeated if it is short, the
+        # last call cut to an evenly spaced subset of its rows to stay near
+        # the budget
+        flops, spent, parts = 0.0, 0.0, []
+        for rep in range(1000):
+            for desc, nq, nk, run, flops_of in jobs:
+                left = budget_s - spent
+                if left <= 0.05 * budget_s:
+                    break
+                n = min(nq, max(1, int(left / (per_unit * nk))))
+                rows = (np.arange(nq, dtype=np.int64) if n >= nq
+                        else np.linspace(0, nq - 1, n).astype(np.int64))
+                t0 = time.perf_counter()
+                run(rows)
+                dt = time.perf_counter() - t0
+                spent += dt
+                per_unit = dt / (len(rows) * nk)
+                flops += flops_of(len(rows))
+                parts.append(f"{desc} ({len(rows)}/{nq} rows)")
+            else:
+                continue
+            break
+        return flops, spent, parts
+
+    flops, spent, parts = sample(target_s)
+    threads = orc.num_threads()
+    orc.set_num_threads(1)
+    try:
+        flops1, spent1, _ = sample(target_s / 3)
+    finally:
+        orc.set_num_threads(threads)
     if len(parts) > 6:
         parts = parts[:3] + [f"... {len(parts) - 6} more calls ..."] + parts[-3:]
     return {
         "value": flops / spent / 1e12,
         "unit": "TFLOP/s",
-        "cores": orc.num_threads(),
+        "cores": threads,
         "kind": "oracle",
         "sample": "; ".join(parts) + f"; all {w.B * w.H} (batch, head) pairs, fp64,"
                   f" {spent:.1f} s",
+        "one_thread_value": flops1 / spent1 / 1e12,
+        "one_thread_sample_s": round(spent1, 1),
     }
 
 
@@ -232,9 +246,11 @@ def main():
 
     kinds = {}
     for g, (kind, a, b) in enumerate(groups):
-        d = kinds.setdefault(kind, {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        d = kinds.setdefault(kind, {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0, "per_step": []})
         for s in range(args.steps):
-            d["ms"] += ev[s][g][0].elapsed_time(ev[s][g][1])
+            ms = ev[s][g][0].elapsed_time(ev[s][g][1])
+            d["ms"] += ms
+            d["per_step"].append(ms * 1e3 / (b - a))
         d["launches"] += (b - a) * args.steps
         for _, _, flops, nbytes in calls[a:b]:
             d["flops"] += flops * args.steps
@@ -243,7 +259,9 @@ def main():
     kern = {}
     for kind, d in kinds.items():
         avg_us = d["ms"] * 1e3 / d["launches"]
-        e = {"launches_per_step": d["launches"] // args.steps, "avg_us": round(avg_us, 3)}
+        ps = sorted(d["per_step"])
+        e = {"launches_per_step": d["launches"] // args.steps, "avg_us": round(avg_us, 3),
+             "median_us": round(ps[len(ps) // 2], 3), "min_us": round(ps[0], 3)}
         if d["flops"]:
             tf = d["flops"] / (d["ms"] / 1e3) / 1e12
             e.update(tflops=round(tf, 2), frac_peak=round(tf / peak, 4))
