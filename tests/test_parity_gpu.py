@@ -235,29 +235,30 @@ def test_chunks_then_merge_equal_full(orc, torch, tile_shape, dtype, d):
     check_lse(to_np(lse), ml, dtype, "merge lse vs oracle merge")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 8, 9, 17, 64])
-def test_merge_many_partials(orc, torch, n):
+def test_merge_many_partials(orc, torch, dtype, n):
     """Every partial count the library compiles a form for (2, 3, 4, 6, 8),
     counts that take the general form (5; above one group of in-flight loads,
     9 and 17; the most one call accepts, 64); a third of the partials empty."""
     B, Nq, H, d = 1, 45, 3, 72
     outs, lses, outs_np, lses_np = [], [], [], []
     for r in range(n):
-        o = random_io((B, Nq, H, d), "bf16", 600 + r)
+        o = random_io((B, Nq, H, d), dtype, 600 + r)
         l = (random_io((B, H, Nq), "f32", 700 + r) * 3).astype(np.float32)
         if r % 3 == 1:
             l[:] = -np.inf
         outs_np.append(o)
         lses_np.append(l)
-        outs.append(to_gpu(o, "bf16"))
+        outs.append(to_gpu(o, dtype))
         lses.append(torch.from_numpy(l).cuda())
-    out = _empty_out(torch, B, Nq, H, d, "bf16")
+    out = _empty_out(torch, B, Nq, H, d, dtype)
     lse = _lse_buf(torch, B, H, Nq)
     xd.xdit_lse_merge(outs, lses, n, out, lse)
     torch.cuda.synchronize()
     mo, ml = orc.merge(outs_np, lses_np)
-    check_out(to_np(out), mo, "bf16", f"merge of {n}")
-    check_lse(to_np(lse), ml, "bf16", f"merge lse of {n}")
+    check_out(to_np(out), mo, dtype, f"merge of {n}")
+    check_lse(to_np(lse), ml, dtype, f"merge lse of {n}")
 
 
 def test_merge_single_partial_is_copy(torch):
