@@ -83,8 +83,8 @@ typedef enum {
  *   fresh_k, fresh_v [B, patch_len, H, d]
  *   out      [B, patch_len, H, d]   attention output
  * Requires 0 <= patch_off, 0 <= patch_len, patch_off + patch_len <= seq_len.
- * patch_len = 0 is a no-op.  out must not overlap any input; fresh_k/fresh_v
- * must not overlap kv_buf.
+ * patch_len = 0 is a no-op.  out must not overlap any input; q, fresh_k and
+ * fresh_v must not overlap kv_buf (the buffer is written while they are read).
  */
 int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patch_len,
                     const void* fresh_k, const void* fresh_v, void* out,
@@ -116,8 +116,8 @@ int xdit_patch_attn(const void* q, void* kv_buf, int64_t patch_off, int64_t patc
  *   out        [B, q_len, H, d]
  *   lse        [B, H, q_len] float32, or NULL
  * q_len = 0 performs only the update; F = 0 is plain attention over the
- * buffer.  out and lse must not overlap any input or each other; the fresh
- * rows must not overlap kv_buf.
+ * buffer.  out and lse must not overlap any input or each other; q and the
+ * fresh rows must not overlap kv_buf.
  */
 int xdit_patch_attn_ranges(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
                            const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
@@ -204,9 +204,13 @@ int xdit_lse_merge(const void* const* outs, const float* const* lses, int32_t n,
  *              overlapping any argument; unused (may be NULL) when no cut
  *              happens.  Its contents on entry do not matter.
  * xdit_split_workspace_bytes returns 0 when the sizes lead to no cut, -1 for
- * sizes or splits the calls reject.  float32 calls run unsplit.  Other
- * arguments as for the unsplit calls.  The sweep and the fix-up are two
- * launches on the calling thread's stream.
+ * sizes or splits the calls reject.  float32 calls, and calls whose sweeps
+ * hold one K/V tile or less (128 keys at d <= 72, 64 at d = 128), run
+ * unsplit.  Other arguments as for the unsplit calls.  The sweep and the
+ * fix-up are two launches on the calling thread's stream.
+ * xdit_chunk_attn_accum_split is the same for the ring step
+ * xdit_chunk_attn_accum: the fix-up merges each cut sweep's result into the
+ * running (out, lse) as the unsplit call does.
  */
 int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
                                    int64_t head_dim, int32_t dtype, int32_t splits);
@@ -214,6 +218,10 @@ int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out
                           int32_t splits, void* workspace, int64_t workspace_bytes, int64_t batch,
                           int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
                           int32_t dtype);
+int xdit_chunk_attn_accum_split(const void* q, const void* k, const void* v, void* out, float* lse,
+                                int32_t splits, void* workspace, int64_t workspace_bytes,
+                                int64_t batch, int64_t q_len, int64_t kv_len, int64_t heads,
+                                int64_t head_dim, int32_t dtype);
 int xdit_patch_attn_split(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,
                           const int64_t* range_off, const int64_t* range_len, const void* fresh_k,
                           const void* fresh_v, void* out, float* lse, int32_t splits,

@@ -17,7 +17,8 @@ from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XDIT
                    XditError, check, lib)
 
 __all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
-           "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
+           "xdit_chunk_attn_accum", "xdit_chunk_attn_accum_split", "xdit_chunk_attn_split",
+           "xdit_patch_attn_split",
            "split_workspace_bytes", "xdit_lse_merge",
            "xdit_kv_update", "xdit_stage_step", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
            "version"]
@@ -201,6 +202,17 @@ def xdit_chunk_attn_accum(q, k, v, out, lse) -> None:
     args = _chunk_args(q, k, v, out, lse)
     _use_current_stream()
     check(lib().xdit_chunk_attn_accum(*args))
+
+
+def xdit_chunk_attn_accum_split(q, k, v, out, lse, splits: int = 0, workspace=None) -> None:
+    """xdit_chunk_attn_accum with each query tile's keys split `splits` ways
+    (0: the library chooses); workspace as for xdit_chunk_attn_split."""
+    if lse is None:
+        raise XditError(-1, "the running lse is required")
+    args = _chunk_args(q, k, v, out, lse)
+    wp, wb = _workspace(workspace)
+    _use_current_stream()
+    check(lib().xdit_chunk_attn_accum_split(*args[:5], int(splits), wp, wb, *args[5:]))
 
 
 def xdit_lse_merge(outs, lses, n: int, out, lse_out=None) -> None:

@@ -41,6 +41,8 @@ SIGNATURES = {
                                              _i32, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn_accum": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
                                              _i32]),
+    "xdit_chunk_attn_accum_split": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _i64,
+                                                   _i64, _i64, _i64, _i64, _i32]),
     "xdit_lse_merge": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_kv_update": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp, _i64, _i64, _i64, _i64, _i32]),
     "xdit_stage_step": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp,

@@ -1024,12 +1024,17 @@ __global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
 // ranges x*s_al .. x*s_al + s_al - 1.  Otherwise workgroup x handles the
 // boundary between ranges x and x + 1 when it falls inside a sweep and is
 // the first boundary inside it, and finds the ranges that meet that sweep.
+// A sweep with a single non-empty part was swept whole by that part, which
+// wrote out and lse itself (no slot): such a sweep is left alone.
+// With accum, the merged chunk result is merged in turn into the running
+// (out, lse), as the sweep kernel's epilogue does for whole sweeps.
 // Thread t: row 16rb + t % 16, dim chunks t / 16, t / 16 + 16, ...
 struct FixArgs {
     uint16_t* out;
     float* lse;
     const float* part;
     int B, H, Nq, q_tiles, T, G2, s_al;
+    int accum;
     int64_t base, rem;  // the cut ranges split units [base, base + rem)
 };
 
@@ -1077,11 +1082,20 @@ __global__ __launch_bounds__(256) void fixup_kernel(FixArgs a) {
     }
     __syncthreads();
     const int n = sh_n;
-    if (n == 0) return;
+    // no cut sweep here, or one part that swept it whole (and wrote it)
+    if (n <= 1) return;
     const int64_t P = sh_pair;
     const int qt = (int)(P % a.q_tiles), bh = (int)(P / a.q_tiles), hh = bh % a.H, b = bh / a.H;
     const int r = kFixRows * blockIdx.y + (int)threadIdx.x % kFixRows, dg = (int)threadIdx.x / kFixRows;
     const int qrow = qt * BM + r;
+    const int64_t lidx = ((int64_t)b * a.H + hh) * a.Nq + qrow;
+    // the running LSE of the row is read by every thread of the row before
+    // the row's first thread overwrites it
+    float lse_prev = -INFINITY;
+    if (a.accum) {
+        if (qrow < a.Nq) lse_prev = a.lse[lidx];
+        __syncthreads();
+    }
     if (qrow >= a.Nq) return;
     constexpr int SLOT = BM * (D + 1);
     // every load of the thread issued up front (parts beyond n predicated
@@ -1121,12 +1135,41 @@ __global__ __launch_bounds__(256) void fixup_kernel(FixArgs a) {
             if (i < n && dg + NG * kk < C4) acc[kk] += w * x[i][kk];
     }
     uint16_t* orow = a.out + (((int64_t)b * a.Nq + qrow) * a.H + hh) * D;
+    // merge into the running state: weights e^{lse_prev - L2}, e^{L - L2}
+    // with L2 = ln(e^{lse_prev} + e^{L}); an empty running state (-inf)
+    // is ignored, an empty chunk (L = -inf) leaves the state as it is
+    float w_prev = 0.f, w_new = 1.f, L_out = L;
+    if (a.accum && lse_prev != -INFINITY) {
+        if (L == -INFINITY) {
+            w_prev = 1.f;
+            w_new = 0.f;
+            L_out = lse_prev;
+        } else {
+            const float M2 = fmaxf(lse_prev, L);
+            const float e1 = __expf(lse_prev - M2), e2 = __expf(L - M2);
+            const float rs = 1.f / (e1 + e2);
+            w_prev = e1 * rs;
+            w_new = e2 * rs;
+            L_out = M2 + __logf(e1 + e2);
+        }
+    }
 #pragma unroll
     for (int kk = 0; kk < PER; ++kk)
-        if (dg + NG * kk < C4)
-            ((u32x2_t*)orow)[dg + NG * kk] =
-                u32x2_t{pack_bf16x2(acc[kk][0], acc[kk][1]), pack_bf16x2(acc[kk][2], acc[kk][3])};
-    if (a.lse && dg == 0) a.lse[((int64_t)b * a.H + hh) * a.Nq + qrow] = L;
+        if (dg + NG * kk < C4) {
+            u32x2_t* dst = (u32x2_t*)orow + dg + NG * kk;
+            f32x4_t y = acc[kk] * w_new;
+            if (w_prev != 0.f) {
+                const u32x2_t pv = *dst;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t h = pv[e >> 1];
+                    const float x0 = __uint_as_float((e & 1) ? (h & 0xffff0000u) : (h << 16));
+                    y[e] = __builtin_fmaf(w_prev, x0, y[e]);
+                }
+            }
+            *dst = u32x2_t{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+        }
+    if (a.lse && dg == 0) a.lse[lidx] = L_out;
 }
 
 template <int D, int QB, int KS, int KW, bool PATCH>
@@ -1165,7 +1208,6 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     a.part = p.part;
     if (pairs == 0) return hipSuccess;
     const bool parts = p.parts > 0;
-    if (parts && p.accum) return hipErrorInvalidValue;  // the fix-up does not merge into a running state
     if (!parts) {
         hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, false>), dim3((unsigned)pairs), dim3(C::THREADS),
                            0, s, a);
@@ -1194,6 +1236,10 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
         f.rem = a.units - f.base;
         const int64_t cut = pairs - p.whole;  // query tiles in the cut ranges
         f.s_al = p.parts % cut == 0 ? (int)(p.parts / cut) : 0;
+        f.accum = p.accum;
+        // one part per cut query tile, or sweeps of one tile: every part
+        // swept its query tile whole and wrote it, nothing to merge
+        if (f.s_al == 1 || a.T == 1) return hipSuccess;
         const int64_t gx = f.s_al > 0 ? cut : p.parts - 1;
         hipLaunchKernelGGL((fixup_kernel<D, C::BM>), dim3((unsigned)gx, C::BM / kFixRows), dim3(256), 0, s, f);
         return hipGetLastError();

@@ -210,18 +210,27 @@ static Partition pick_parts(int64_t pairs, int64_t kv_len, int64_t head_dim) {
     return best < 0.9 * plain ? pick : none;
 }
 
+// The partition of a call: none for float32 (not partitioned) or for
+// sweeps of at most one K/V tile (nothing to cut: a part would sweep its
+// query tile whole), every sweep in `splits` even parts for splits > 1, the
+// library's choice for splits <= 0.
+static Partition call_parts(int32_t dtype, int64_t pairs, int64_t kv_len, int64_t head_dim, int32_t splits) {
+    Partition pt;
+    const int64_t bn = head_dim > 96 ? 64 : 128;  // kernel K/V tile of a partitioned launch
+    if (dtype != XDIT_BF16 || pairs == 0 || kv_len <= bn) return pt;
+    if (splits > 1) pt.parts = pairs * splits;
+    else if (splits <= 0) pt = pick_parts(pairs, kv_len, head_dim);
+    return pt;
+}
+
 // Resolve the partition and check the workspace; returns XDIT_OK and sets
 // *pt_out.
 static int resolve_parts(const char* fn, const SplitArgs& sa, int32_t dtype, int64_t batch, int64_t q_len,
                          int64_t kv_len, int64_t heads, int64_t head_dim, Partition* pt_out) {
     if (sa.splits > XDIT_MAX_SPLITS)
         return fail(XDIT_ERR_RANGE, "%s: splits = %d above %d", fn, sa.splits, XDIT_MAX_SPLITS);
-    Partition pt;
     const int64_t pairs = part_pairs(batch, q_len, heads);
-    if (dtype == XDIT_BF16 && pairs > 0) {  // the float32 path is not partitioned
-        if (sa.splits > 1) pt.parts = pairs * sa.splits;
-        else if (sa.splits <= 0) pt = pick_parts(pairs, kv_len, head_dim);
-    }
+    const Partition pt = call_parts(dtype, pairs, kv_len, head_dim, sa.splits);
     if (pt.parts > 0) {
         const int64_t need = part_ws_bytes(pt, pairs, head_dim);
         if (sa.workspace == nullptr || sa.workspace_bytes < need)
@@ -321,8 +330,10 @@ static int check_patch_args(const char* fn, const void* q, void* kv_buf, int64_t
         sk{fresh_k, batch * patch_len * row, "fresh_k"}, sv{fresh_v, batch * patch_len * row, "fresh_v"},
         sq{q, q ? batch * patch_len * row : 0, "q"}, so{out, out ? batch * patch_len * row : 0, "out"};
     for (const Span* s : {&sb, &sk, &sv, &sq, &so}) XDIT_TRY(check_ptr(*s));
+    // the buffer is written while the queries and fresh rows are read
     XDIT_TRY(check_no_overlap(sk, sb));
     XDIT_TRY(check_no_overlap(sv, sb));
+    XDIT_TRY(check_no_overlap(sq, sb));
     for (const Span* s : {&sq, &sb, &sk, &sv}) XDIT_TRY(check_no_overlap(so, *s));
     return XDIT_OK;
 }
@@ -362,8 +373,10 @@ static int patch_ranges_impl(const char* fn, const void* q, int64_t q_len, void*
         so{out, batch * q_len * row, "out"}, sl{lse, lse ? batch * heads * q_len * 4 : 0, "lse"};
     for (const Span* s : {&sb, &sk, &sv, &sq, &so}) XDIT_TRY(check_ptr(*s));
     if (lse && ((uintptr_t)lse & 3u)) return fail(XDIT_ERR_LAYOUT, "lse is not 4-byte aligned");
+    // the buffer is written while the queries and fresh rows are read
     XDIT_TRY(check_no_overlap(sk, sb));
     XDIT_TRY(check_no_overlap(sv, sb));
+    XDIT_TRY(check_no_overlap(sq, sb));
     for (const Span* s : {&sq, &sb, &sk, &sv}) {
         XDIT_TRY(check_no_overlap(so, *s));
         XDIT_TRY(check_no_overlap(sl, *s));
@@ -460,11 +473,7 @@ int64_t xdit_split_workspace_bytes(int64_t batch, int64_t q_len, int64_t kv_len,
     if (check_dims("xdit_split_workspace_bytes", batch, q_len, kv_len, heads) != XDIT_OK) return -1;
     if (splits > XDIT_MAX_SPLITS) return -1;
     const int64_t pairs = part_pairs(batch, q_len, heads);
-    if (dtype != XDIT_BF16 || pairs == 0) return 0;
-    Partition pt;
-    if (splits > 1) pt.parts = pairs * splits;
-    else if (splits <= 0) pt = pick_parts(pairs, kv_len, head_dim);
-    return part_ws_bytes(pt, pairs, head_dim);
+    return part_ws_bytes(call_parts(dtype, pairs, kv_len, head_dim, splits), pairs, head_dim);
 }
 
 int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out, float* lse,
@@ -478,6 +487,19 @@ int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out
     sa.workspace_bytes = workspace_bytes;
     return chunk_impl("xdit_chunk_attn_split", q, k, v, out, lse, batch, q_len, kv_len, heads,
                       head_dim, dtype, 0, sa);
+}
+
+int xdit_chunk_attn_accum_split(const void* q, const void* k, const void* v, void* out, float* lse,
+                                int32_t splits, void* workspace, int64_t workspace_bytes, int64_t batch,
+                                int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
+                                int32_t dtype) {
+    clear_error();
+    SplitArgs sa;
+    sa.splits = splits;
+    sa.workspace = workspace;
+    sa.workspace_bytes = workspace_bytes;
+    return chunk_impl("xdit_chunk_attn_accum_split", q, k, v, out, lse, batch, q_len, kv_len, heads,
+                      head_dim, dtype, 1, sa);
 }
 
 int xdit_patch_attn_split(const void* q, int64_t q_len, void* kv_buf, int32_t n_ranges,

@@ -22,8 +22,8 @@ from __future__ import annotations
 import numpy as np
 
 from . import (split_workspace_bytes, xdit_chunk_attn, xdit_chunk_attn_accum,
-               xdit_chunk_attn_split, xdit_lse_merge, xdit_patch_attn, xdit_patch_attn_ranges,
-               xdit_patch_attn_split, xdit_stage_step)
+               xdit_chunk_attn_accum_split, xdit_chunk_attn_split, xdit_lse_merge, xdit_patch_attn,
+               xdit_patch_attn_ranges, xdit_patch_attn_split, xdit_stage_step)
 from .inputs import Tensors, Workload
 
 
@@ -91,7 +91,7 @@ class HotPath:
                 n = split_workspace_bytes(self.patch_q[p], w.N)
                 self.patch_split[p] = n > 0
                 need = max(need, n)
-            if self.sp_q is not None and not w.sp_ring:
+            if self.sp_q is not None:
                 for s_, e_ in w.sp_chunks:
                     n = split_workspace_bytes(self.sp_q, e_ - s_)
                     self.chunk_split = self.chunk_split or n > 0
@@ -123,8 +123,13 @@ class HotPath:
         if self.w.sp_ring:
             # ring form: the first chunk starts the running (out, lse), the
             # others are merged into it
-            f = xdit_chunk_attn if r == 0 else xdit_chunk_attn_accum
-            f(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.sp_out, self.sp_lse)
+            if self.chunk_split:
+                f = xdit_chunk_attn_split if r == 0 else xdit_chunk_attn_accum_split
+                f(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.sp_out, self.sp_lse, 0,
+                  self.workspace)
+            else:
+                f = xdit_chunk_attn if r == 0 else xdit_chunk_attn_accum
+                f(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.sp_out, self.sp_lse)
         elif self.chunk_split:
             xdit_chunk_attn_split(self.sp_q, self.chunk_k[r], self.chunk_v[r], self.chunk_out[r],
                                   self.chunk_lse[r], 0, self.workspace)

@@ -28,7 +28,8 @@ def header_functions():
 def test_header_declares_the_entry_points():
     names = header_functions()
     for fn in ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
-               "xdit_chunk_attn_accum", "xdit_chunk_attn_split", "xdit_patch_attn_split",
+               "xdit_chunk_attn_accum", "xdit_chunk_attn_accum_split", "xdit_chunk_attn_split",
+               "xdit_patch_attn_split",
                "xdit_split_workspace_bytes", "xdit_lse_merge", "xdit_kv_update", "xdit_stage_step",
                "xdit_set_stream",
                "xdit_get_stream", "xdit_last_error", "xdit_version"]:
@@ -94,6 +95,8 @@ def P(i):
     (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(1), 1, 16, 2, 64, 0), -6),
     (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(0), 1, 16, 2, 64, 0), -6),
     (lambda L: L.xdit_patch_attn(P(0), P(1), 0, 8, P(2), P(3), P(4), 1, 16, 2, 72, 3), -2),
+    # q inside the buffer: the buffer's slice is written while queries load
+    (lambda L: L.xdit_patch_attn(P(1) + 4096, P(1), 0, 8, P(2), P(3), P(4), 1, 16, 2, 64, 0), -6),
     (lambda L: L.xdit_kv_update(P(1), 9, 8, P(2), P(3), 1, 16, 2, 64, 0), -4),
     (lambda L: L.xdit_kv_update(P(1), 0, 8, P(2) + 4, P(3), 1, 16, 2, 64, 0), -5),
     (lambda L: L.xdit_kv_update(P(1), 0, 8, P(2), P(1) + 2 * 16 * 128 * 2 - 16, 1, 16, 2, 64, 0), -6),
@@ -149,6 +152,14 @@ def test_ranges_rejections(ranges, q_len, fk, out, lse, code):
     assert lib.xdit_last_error().decode(), "no message for a rejected call"
 
 
+@needs_no_gpu
+def test_ranges_rejects_queries_inside_the_buffer():
+    lib = _lib.lib()
+    n, offs, lens = _ranges((0, 4))
+    assert lib.xdit_patch_attn_ranges(P(1) + 2048, 8, P(1), n, offs, lens, P(2), P(3), P(4), P(5),
+                                      1, 16, 2, 64, 0) == -6
+
+
 def test_split_workspace_bytes():
     """Partitioned launches keep one float32 partial slot (128 query rows x
     (d + 1)) per cut range, two when ranges may cross query tiles."""
@@ -173,6 +184,13 @@ def test_split_workspace_bytes():
     assert lib.xdit_split_workspace_bytes(1, 4224, 4224, 24, 128, 0, 0) == 240 * slot(128)
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 64, 0, 17) == -1
     assert lib.xdit_split_workspace_bytes(2, 512, 4429, 24, 80, 0, 2) == -1
+    # sweeps of one K/V tile or none (128 keys at d <= 72, 64 at d = 128)
+    # have nothing to cut: any split runs unsplit
+    for d, nk in ((64, 0), (64, 1), (64, 128), (72, 100), (128, 64)):
+        for splits in (2, 16, 0):
+            assert lib.xdit_split_workspace_bytes(1, 200, nk, 3, d, 0, splits) == 0, (d, nk, splits)
+    assert lib.xdit_split_workspace_bytes(1, 200, 129, 3, 64, 0, 2) == 2 * 6 * slot(64)
+    assert lib.xdit_split_workspace_bytes(1, 200, 65, 3, 128, 0, 2) == 2 * 6 * slot(128)
 
 
 @needs_no_gpu
@@ -192,6 +210,13 @@ def test_split_rejections():
     n, offs, lens = _ranges((0, 8))
     assert lib.xdit_patch_attn_split(P(0), 8, P(1), n, offs, lens, P(2), P(3), P(4), None, 4,
                                      P(1) + 4096, need, 1, 1024, 2, 64, 0) == -6
+    # the ring step's split form: the running lse is required, the workspace checked
+    assert lib.xdit_chunk_attn_accum_split(P(0), P(1), P(2), P(3), None, 4, P(5), need,
+                                           1, 16, 1024, 2, 64, 0) == -1
+    assert lib.xdit_chunk_attn_accum_split(P(0), P(1), P(2), P(3), P(4), 4, P(5), need - 1,
+                                           1, 16, 1024, 2, 64, 0) == -4
+    assert lib.xdit_chunk_attn_accum_split(P(0), P(1), P(2), P(3), P(4), 4, P(4), need,
+                                           1, 16, 1024, 2, 64, 0) == -6
 
 
 @needs_no_gpu
