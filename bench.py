@@ -17,8 +17,13 @@ Prints ONE JSON line.
 
 `value` is algorithmic attention FLOP/s (4*B*H*Nq*Nk*d per call) over the
 whole step.  `roofline` refers to the kernel with the largest share of the
-step's time.  `cpu_baseline` times the fp64 oracle on a bounded row sample of
-the same workload on the host's cores.
+step's time: `achieved` and `frac` are timed with HIP events live in this
+run; `traffic` (HBM bytes) and `mfma_busy` come from rocprofv3 counter runs
+of the same kernel build, named in `traffic_source`, and are null for any
+other build.  `cpu_baseline` times the fp64 oracle on a bounded row sample of
+the same workload on the host's cores.  With the default pixart workload the
+line also carries `flux_16k`: the same measurement of the Flux 2048px
+sequence-parallel share (16896 tokens), the 16k-token configuration.
 """
 from __future__ import annotations
 
@@ -61,6 +66,23 @@ def traffic_of(workload: str, kind: str):
     return e["bytes"] if kernel_fingerprint() == e["src"] else None
 
 
+# Matrix-core counters of the dominant kernel from a rocprofv3 --pmc run of
+# the same workload (SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES):
+# the fraction of the kernel's CU-busy time the matrix pipes worked), with the
+# summary file and the kernel build's fingerprint; a different build reports
+# nothing.
+MEASURED_COUNTERS = {}
+
+
+def counters_of(workload: str, kind: str) -> dict:
+    from paper_2411_01738_amd.build import kernel_fingerprint
+
+    e = MEASURED_COUNTERS.get((workload, kind))
+    if e is None or kernel_fingerprint() != e["src"]:
+        return {"traffic_source": None, "mfma_busy": None}
+    return {"traffic_source": e["file"], "mfma_busy": e["mfma_busy"]}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -72,17 +94,20 @@ def parse():
                              "flux_ring"])
     ap.add_argument("--no-split", action="store_true",
                     help="never split a query tile's keys over several workgroups")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
+    ap.add_argument("--no-flux", action="store_true",
+                    help="with the pixart workload, skip the Flux 16k-token SP share beside it")
     return ap.parse_args()
 
 
-def cpu_baseline(w, t, target_s: float):
+def cpu_baseline(w, t, target_s: float, one_thread: bool = True):
     """fp64 oracle on a bounded sample of the workload: whole calls of the step
-    in order (patch steps, else chunk steps) until about target_s seconds have
-    been spent; when one call alone would take far longer, an evenly spaced
-    subset of its query rows.  Scaled to TFLOP/s of algorithmic work.  The
-    same is then run on one thread for a third of the time."""
+    in order (patch steps, else chunk steps) until about target_s / 3 seconds
+    have been spent; when one call alone would take far longer, an evenly
+    spaced subset of its query rows.  Scaled to TFLOP/s of algorithmic work;
+    the median of 3 such samples is reported.  With one_thread, the same is
+    then run on one thread for a quarter of the time."""
     import numpy as np
 
     import oracle
@@ -153,48 +178,58 @@ def cpu_baseline(w, t, target_s: float):
             break
         return flops, spent, parts
 
-    flops, spent, parts = sample(target_s)
+    runs = [sample(target_s / 3) for _ in range(3)]
+    rates = [f / sp / 1e12 for f, sp, _ in runs]
+    med = sorted(range(3), key=lambda i: rates[i])[1]
+    flops, spent, parts = runs[med]
     threads = orc.num_threads()
-    orc.set_num_threads(1)
-    try:
-        flops1, spent1, _ = sample(target_s / 3)
-    finally:
-        orc.set_num_threads(threads)
     if len(parts) > 6:
         parts = parts[:3] + [f"... {len(parts) - 6} more calls ..."] + parts[-3:]
-    return {
-        "value": flops / spent / 1e12,
+    out = {
+        "value": rates[med],
         "unit": "TFLOP/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": "; ".join(parts) + f"; all {w.B * w.H} (batch, head) pairs, fp64,"
-                  f" {spent:.1f} s",
-        "one_thread_value": flops1 / spent1 / 1e12,
-        "one_thread_sample_s": round(spent1, 1),
+        "sample": "median of 3 samples, each: " + "; ".join(parts) +
+                  f"; all {w.B * w.H} (batch, head) pairs, fp64, {spent:.1f} s",
+        "samples_tflops": [round(r, 5) for r in rates],
+        "cpu": cpu_model(),
     }
+    if one_thread:
+        orc.set_num_threads(1)
+        try:
+            flops1, spent1, _ = sample(target_s / 4)
+        finally:
+            orc.set_num_threads(threads)
+        out["one_thread_value"] = flops1 / spent1 / 1e12
+        out["one_thread_sample_s"] = round(spent1, 1)
+    return out
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(this build has no multi-GPU path)", file=sys.stderr)
-        sys.exit(2)
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
+
+def measure(w, t, steps: int, warmup: int, split: bool, extra_timings: bool = True):
+    """Time one workload on the GPU: `warmup` untimed steps, then exactly
+    `steps` timed steps between synchronisations (events only at the two
+    ends), then `steps` more with HIP events around each run of consecutive
+    launches of one kernel.  Returns the step figures, per-kernel figures and
+    the roofline of the kernel with the largest share of the step."""
     import torch
 
     from paper_2411_01738_amd import _lib
     from paper_2411_01738_amd.hotpath import HotPath
-    from paper_2411_01738_amd.inputs import WORKLOADS, generate
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    _lib.lib()  # fails loudly if the HIP library is missing
-    torch.cuda.set_device(0)
-    w = WORKLOADS[args.workload]
-    t = generate(w)
-    hp = HotPath(w, t, split=not args.no_split)
+    hp = HotPath(w, t, split=split)
     stream = torch.cuda.current_stream()
 
     # each entry: (kind, callable, flops, bytes)
@@ -208,7 +243,7 @@ def main():
         if not w.sp_ring:
             calls.append(("lse_merge", hp.merge, 0.0, hp.merge_bytes()))
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         hp.step()
     torch.cuda.synchronize()
 
@@ -216,12 +251,12 @@ def main():
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         for _, fn, _, _ in calls:
             fn()
     end.record(stream)
     torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
+    ms_per_step = start.elapsed_time(end) / steps
 
     # per-kernel durations: K more steps with HIP events on the launch stream
     # around each run of consecutive launches of one kernel (the M patch
@@ -234,33 +269,33 @@ def main():
         else:
             groups.append([kind, i, i + 1])
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in groups] for _ in range(args.steps)]
+           for _ in groups] for _ in range(steps)]
     torch.cuda.synchronize()
-    for s in range(args.steps):
+    for s_ in range(steps):
         for g, (_, a, b) in enumerate(groups):
-            ev[s][g][0].record(stream)
+            ev[s_][g][0].record(stream)
             for _, fn, _, _ in calls[a:b]:
                 fn()
-            ev[s][g][1].record(stream)
+            ev[s_][g][1].record(stream)
     torch.cuda.synchronize()
 
     kinds = {}
     for g, (kind, a, b) in enumerate(groups):
         d = kinds.setdefault(kind, {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0, "per_step": []})
-        for s in range(args.steps):
-            ms = ev[s][g][0].elapsed_time(ev[s][g][1])
+        for s_ in range(steps):
+            ms = ev[s_][g][0].elapsed_time(ev[s_][g][1])
             d["ms"] += ms
             d["per_step"].append(ms * 1e3 / (b - a))
-        d["launches"] += (b - a) * args.steps
+        d["launches"] += (b - a) * steps
         for _, _, flops, nbytes in calls[a:b]:
-            d["flops"] += flops * args.steps
-            d["bytes"] += nbytes * args.steps
+            d["flops"] += flops * steps
+            d["bytes"] += nbytes * steps
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     kern = {}
     for kind, d in kinds.items():
         avg_us = d["ms"] * 1e3 / d["launches"]
         ps = sorted(d["per_step"])
-        e = {"launches_per_step": d["launches"] // args.steps, "avg_us": round(avg_us, 3),
+        e = {"launches_per_step": d["launches"] // steps, "avg_us": round(avg_us, 3),
              "median_us": round(ps[len(ps) // 2], 3), "min_us": round(ps[0], 3)}
         if d["flops"]:
             tf = d["flops"] / (d["ms"] / 1e3) / 1e12
@@ -275,7 +310,7 @@ def main():
     # marshalled once (a launch takes less time than the binding's checks).
     # Cold: each launch after a 1 GiB write that evicts L2 and the MALL,
     # bracketed by its own events (which add about a microsecond).
-    if w.patches():
+    if extra_timings and w.patches():
         off, ln = w.patches()[0]
         L = _lib.lib()
         L.xdit_set_stream(stream.cuda_stream)
@@ -313,7 +348,7 @@ def main():
 
     # the merge is one launch per step, so its in-step events include their
     # own overhead; back-to-back launches through the C ABI give its duration
-    if hp.sp_q is not None and not w.sp_ring:
+    if extra_timings and hp.sp_q is not None and not w.sp_ring:
         import ctypes
 
         L = _lib.lib()
@@ -357,6 +392,9 @@ def main():
     dom = max(kinds, key=lambda k: kinds[k]["ms"])
     dd = kinds[dom]
     avg_s = dd["ms"] / 1e3 / dd["launches"]
+    timing = ("HIP events on the launch stream around each run of launches of this kernel,"
+              " over the K steps after the timed region; achieved = algorithmic work per launch"
+              " / average launch duration")
     if dd["flops"]:
         per_launch = dd["flops"] / dd["launches"]
         achieved = per_launch / avg_s / 1e12
@@ -370,52 +408,99 @@ def main():
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     roof["traffic"] = traffic_of(w.name, dom)
+    roof["timing"] = timing
+    roof.update(counters_of(w.name, dom))
+    hp = None
+    torch.cuda.empty_cache()
+    return {"ms_per_step": ms_per_step, "value": value, "step_flops": step_flops, "kernels": kern,
+            "roofline": roof}
+
+
+DESC = {"tiny": "tiny fp32: B=1 H=2 d=64, 256 tokens, M=4 patch steps + 4-chunk SP share",
+        "pixart": "pixart-1024px: B=2 H=16 d=72, 4096 tokens, M=4 patch steps"
+                  " + 4-chunk SP share (Q 1024 rows)",
+        "sd3": "sd3-1024px joint attention: B=2 H=24 d=64, 4096 image + 333 text tokens,"
+               " M=8 patch steps",
+        "flux": "flux-2048px SP share: B=1 H=24 d=128, Q 4224 rows x 4 chunks of 4224 + merge",
+        "cog": "cogvideox video: B=1 H=48 d=64, 17550 video + 226 text tokens, M=16 patch"
+               " steps + 8-chunk split (Q all rows) + merge",
+        "sd3_ic": "sd3-1024px in-context: B=2 H=24 d=64, 4096 image + 333 text tokens,"
+                  " M=8 patch steps, patch 0 carries the text (845 fresh rows and queries)",
+        "sd3_ic_bal": "sd3-1024px in-context, balanced partition: B=2 H=24 d=64, 4096 image"
+                      " + 333 text tokens, M=8 patch steps of 553-554 fresh rows (patch 0:"
+                      " 220 image + 333 text)",
+        "flux_ring": "flux-2048px SP share, ring form: B=1 H=24 d=128, Q 4224 rows, 4 chunks"
+                     " of 4224 each merged into the running output as it arrives",
+        "pixart_stage": "pixart-1024px stage micro-steps: B=2 H=16 d=72 hidden 1152, 4096"
+                        " tokens, M=4 x (QKV projections, patch step, output projection);"
+                        " value counts projection and attention FLOPs",
+        "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"
+                         " 4096 tokens, M=4 patch steps of 1024 gathered fresh rows,"
+                         " 512 local queries each"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2411_01738_amd import _lib
+    from paper_2411_01738_amd.inputs import WORKLOADS, generate
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    _lib.lib()  # fails loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    w = WORKLOADS[args.workload]
+    t = generate(w)
+    m = measure(w, t, args.steps, args.warmup, not args.no_split)
+
+    # the 16k-token target configuration (Flux SP share) beside the headline
+    # one, under the same clock: same K and W, its own per-kernel figures,
+    # roofline and oracle sample
+    flux = None
+    if args.workload == "pixart" and not args.no_flux:
+        wf = WORKLOADS["flux"]
+        tf = generate(wf)
+        mf = measure(wf, tf, args.steps, args.warmup, not args.no_split, extra_timings=True)
+        flux = {"workload": DESC["flux"], "value": round(mf["value"], 2), "unit": "TFLOP/s",
+                "ms_per_step": round(mf["ms_per_step"], 4), "flops_per_step": mf["step_flops"],
+                "kernels": mf["kernels"], "roofline": mf["roofline"]}
+        if args.cpu_seconds > 0:
+            flux["cpu_baseline"] = cpu_baseline(wf, tf, args.cpu_seconds * 0.6, one_thread=False)
+        del tf
 
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(w, t, args.cpu_seconds)
 
-    desc = {"tiny": "tiny fp32: B=1 H=2 d=64, 256 tokens, M=4 patch steps + 4-chunk SP share",
-            "pixart": "pixart-1024px: B=2 H=16 d=72, 4096 tokens, M=4 patch steps"
-                      " + 4-chunk SP share (Q 1024 rows)",
-            "sd3": "sd3-1024px joint attention: B=2 H=24 d=64, 4096 image + 333 text tokens,"
-                   " M=8 patch steps",
-            "flux": "flux-2048px SP share: B=1 H=24 d=128, Q 4224 rows x 4 chunks of 4224 + merge",
-            "cog": "cogvideox video: B=1 H=48 d=64, 17550 video + 226 text tokens, M=16 patch"
-                   " steps + 8-chunk split (Q all rows) + merge",
-            "sd3_ic": "sd3-1024px in-context: B=2 H=24 d=64, 4096 image + 333 text tokens,"
-                      " M=8 patch steps, patch 0 carries the text (845 fresh rows and queries)",
-            "sd3_ic_bal": "sd3-1024px in-context, balanced partition: B=2 H=24 d=64, 4096 image"
-                          " + 333 text tokens, M=8 patch steps of 553-554 fresh rows (patch 0:"
-                          " 220 image + 333 text)",
-            "flux_ring": "flux-2048px SP share, ring form: B=1 H=24 d=128, Q 4224 rows, 4 chunks"
-                         " of 4224 each merged into the running output as it arrives",
-            "pixart_stage": "pixart-1024px stage micro-steps: B=2 H=16 d=72 hidden 1152, 4096"
-                            " tokens, M=4 x (QKV projections, patch step, output projection);"
-                            " value counts projection and attention FLOPs",
-            "pixart_hybrid": "pixart-1024px PipeFusion x 2-way SP share: B=2 H=16 d=72,"
-                             " 4096 tokens, M=4 patch steps of 1024 gathered fresh rows,"
-                             " 512 local queries each"}[w.name]
     line = {
         "metric": "attention TFLOP/s (bf16) per patch/chunk step; merge GB/s",
-        "value": round(value, 2),
+        "value": round(m["value"], 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(m["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": desc, "B": w.B, "H": w.H, "d": w.d, "tokens": w.N,
+        "config": {"workload": DESC[w.name], "B": w.B, "H": w.H, "d": w.d, "tokens": w.N,
                    "patches": len(w.patches()), "sp_chunks": len(w.sp_chunks),
-                   "flops_per_step": step_flops},
-        "kernels": kern,
-        "roofline": roof,
+                   "flops_per_step": m["step_flops"]},
+        "kernels": m["kernels"],
+        "roofline": m["roofline"],
         "cpu_baseline": cpu,
     }
+    if flux is not None:
+        line["flux_16k"] = flux
     print(json.dumps(line), flush=True)
 
 
