@@ -229,6 +229,29 @@ int xdit_patch_attn_split(const void* q, int64_t q_len, void* kv_buf, int32_t n_
                           int64_t heads, int64_t head_dim, int32_t dtype);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation as xdit_chunk_attn_split, with the partial slots of cut sweeps
+ * kept in a fixed device array inside the library instead of a caller
+ * workspace.  Arguments and results as for xdit_chunk_attn_split without
+ * the workspace.
+ *   Limit: the partition's slots (xdit_split_workspace_bytes for the same
+ *   sizes and splits) must fit in xdit_noalloc_scratch_bytes() bytes
+ *   (16 MiB: the Flux 2048px share, 4224 queries over a 4224-key chunk with
+ *   24 heads of 128, needs 15.9 MB); larger partitions are rejected with
+ *   XDIT_ERR_RANGE before anything is launched.
+ *   The array is one per GPU, allocated when the library is loaded onto it
+ *   and held until the process ends; its device address is looked up on the
+ *   first call on each device.  Every call on a GPU uses that GPU's array:
+ *   calls that overlap on one GPU (other streams, other threads) race on it
+ *   and must be ordered by the caller.  No call allocates or frees memory.
+ */
+int xdit_chunk_attn_split_noalloc(const void* q, const void* k, const void* v, void* out, float* lse,
+                                  int32_t splits, int64_t batch, int64_t q_len, int64_t kv_len,
+                                  int64_t heads, int64_t head_dim, int32_t dtype);
+int64_t xdit_noalloc_scratch_bytes(void);
+
+/*
  * The update half of the patch step on its own (Section 4.1.2): copy the
  * fresh K/V rows into rows [patch_off, patch_off + patch_len) of kv_buf,
  * bit for bit, leaving every other row unchanged.  xdit_patch_attn performs

@@ -18,7 +18,7 @@ from ._lib import (XDIT_BF16, XDIT_F32, XDIT_MAX_PARTIALS, XDIT_MAX_RANGES, XDIT
 
 __all__ = ["xdit_patch_attn", "xdit_patch_attn_ranges", "xdit_chunk_attn",
            "xdit_chunk_attn_accum", "xdit_chunk_attn_accum_split", "xdit_chunk_attn_split",
-           "xdit_patch_attn_split",
+           "xdit_patch_attn_split", "xdit_chunk_attn_split_noalloc",
            "split_workspace_bytes", "xdit_lse_merge",
            "xdit_kv_update", "xdit_stage_step", "set_stream", "XditError", "XDIT_MAX_PARTIALS", "XDIT_MAX_RANGES",
            "version"]
@@ -173,6 +173,14 @@ def xdit_chunk_attn_split(q, k, v, out, lse=None, splits: int = 0, workspace=Non
     wp, wb = _workspace(workspace)
     _use_current_stream()
     check(lib().xdit_chunk_attn_split(*args[:5], int(splits), wp, wb, *args[5:]))
+
+
+def xdit_chunk_attn_split_noalloc(q, k, v, out, lse=None, splits: int = 0) -> None:
+    """xdit_chunk_attn_split with the partials kept in the library's fixed
+    per-GPU scratch array (no workspace, nothing allocated)."""
+    args = _chunk_args(q, k, v, out, lse)
+    _use_current_stream()
+    check(lib().xdit_chunk_attn_split_noalloc(*args[:5], int(splits), *args[5:]))
 
 
 def xdit_patch_attn_split(q, kv_buf, ranges, fresh_k, fresh_v, out, lse=None, splits: int = 0,

@@ -37,6 +37,9 @@ SIGNATURES = {
     "xdit_split_workspace_bytes": (_i64, [_i64, _i64, _i64, _i64, _i64, _i32, _i32]),
     "xdit_chunk_attn_split": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _i64, _i64,
                                              _i64, _i64, _i64, _i32]),
+    "xdit_chunk_attn_split_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i64, _i64, _i64,
+                                                     _i64, _i64, _i32]),
+    "xdit_noalloc_scratch_bytes": (_i64, []),
     "xdit_patch_attn_split": (ctypes.c_int, [_vp, _i64, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                              _i32, _vp, _i64, _i64, _i64, _i64, _i64, _i32]),
     "xdit_chunk_attn_accum": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,

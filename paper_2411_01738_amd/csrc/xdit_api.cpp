@@ -489,6 +489,71 @@ int xdit_chunk_attn_split(const void* q, const void* k, const void* v, void* out
                       head_dim, dtype, 0, sa);
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free form of xdit_chunk_attn_split: the partial slots of cut
+// sweeps live in a fixed device array instead of a caller workspace.  Each
+// GPU the library runs on holds its own copy of the array until the process
+// ends, and every call on that GPU shares it: the kernels write every slot
+// they read within the call, so nothing needs clearing, but two calls that
+// overlap on one GPU (concurrent streams or threads) race on it.
+namespace {
+
+constexpr int64_t kScratchBytes = (int64_t)16 << 20;  // 16 MiB
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.  The array's name is
+// a host-side stand-in in host code: its device address comes from
+// hipGetSymbolAddress, called once per device with that device current.
+int scratch_of_current_device(const char* fn, void** out) {
+    int dev = -1;
+    XDIT_TRY(hip_status(hipGetDevice(&dev), fn));
+    if (dev < 0 || dev >= kMaxDevices) return fail(XDIT_ERR_HIP, "%s: device %d out of range", fn, dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        XDIT_TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), fn));
+        if (p == nullptr) return fail(XDIT_ERR_HIP, "%s: no device address for the scratch array", fn);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return XDIT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t xdit_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+int xdit_chunk_attn_split_noalloc(const void* q, const void* k, const void* v, void* out, float* lse,
+                                  int32_t splits, int64_t batch, int64_t q_len, int64_t kv_len,
+                                  int64_t heads, int64_t head_dim, int32_t dtype) {
+    clear_error();
+    const char* fn = "xdit_chunk_attn_split_noalloc";
+    // size checks first, on the host: the partition's slots must fit
+    XDIT_TRY(check_dtype_dim(dtype, head_dim));
+    XDIT_TRY(check_dims(fn, batch, q_len, kv_len, heads));
+    if (splits > XDIT_MAX_SPLITS)
+        return fail(XDIT_ERR_RANGE, "%s: splits = %d above %d", fn, splits, XDIT_MAX_SPLITS);
+    const int64_t pairs = part_pairs(batch, q_len, heads);
+    const int64_t need = part_ws_bytes(call_parts(dtype, pairs, kv_len, head_dim, splits), pairs, head_dim);
+    if (need > kScratchBytes)
+        return fail(XDIT_ERR_RANGE, "%s: the partition needs %lld bytes of scratch, above the %lld-byte maximum",
+                    fn, (long long)need, (long long)kScratchBytes);
+    SplitArgs sa;
+    sa.splits = splits;
+    sa.workspace_bytes = kScratchBytes;
+    if (need > 0) XDIT_TRY(scratch_of_current_device(fn, &sa.workspace));
+    return chunk_impl(fn, q, k, v, out, lse, batch, q_len, kv_len, heads, head_dim, dtype, 0, sa);
+}
+
 int xdit_chunk_attn_accum_split(const void* q, const void* k, const void* v, void* out, float* lse,
                                 int32_t splits, void* workspace, int64_t workspace_bytes, int64_t batch,
                                 int64_t q_len, int64_t kv_len, int64_t heads, int64_t head_dim,
