@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIBRARY = os.path.join(HERE, "libxdit.so")
-SOURCES = ["xdit_api.cpp", "attn_bf16.hip", "attn_f32.hip", "merge_update.hip"]
+SOURCES = ["xdit_api.cpp", "attn_bf16.hip", "attn_w64.hip", "attn_f32.hip", "merge_update.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -32,15 +32,20 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 EXTRA = {"attn_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]}
 
 
-def kernel_fingerprint(src: str = "attn_bf16.hip") -> str:
-    """sha256 prefix of a source file and its compile flags: measurements
-    taken on one build of a kernel are matched to it by this value."""
+ATTN_SOURCES = ("attn_bf16.hip", "attn_w64.hip", "attn_common.h")
+
+
+def kernel_fingerprint(srcs=ATTN_SOURCES) -> str:
+    """sha256 prefix of the attention kernels' sources and compile flags:
+    measurements taken on one build of the kernels are matched to it by this
+    value."""
     import hashlib
 
     h = hashlib.sha256()
-    with open(os.path.join(CSRC, src), "rb") as f:
-        h.update(f.read())
-    h.update(" ".join(FLAGS + EXTRA.get(src, [])).encode())
+    for src in ([srcs] if isinstance(srcs, str) else srcs):
+        with open(os.path.join(CSRC, src), "rb") as f:
+            h.update(f.read())
+        h.update(" ".join(FLAGS + EXTRA.get(src, [])).encode())
     return h.hexdigest()[:16]
 
 

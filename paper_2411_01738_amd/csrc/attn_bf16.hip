@@ -58,20 +58,8 @@
 namespace xdit {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+#include "attn_common.h"
 
-constexpr uint32_t kOOB = 0x80000000u;  // offset past any buffer's range: reads 0, writes dropped
-constexpr int kRsrcFlags = 0x00020000;  // raw buffer, 32-bit data format
-constexpr float kRescaleLog2 = 8.0f;    // raise the reference max only beyond 2^8 growth
-constexpr int kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
 
 template <int D, int QB_, int KS_, int KW_>
 struct Cfg {
@@ -117,13 +105,19 @@ struct Cfg {
     static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
     // Iteration t reads V of tile t and K of tile t+1 while the tiles after
-    // them load: three stages at least, four where they fit.
-    static constexpr int NSTAGE = kLdsBytes / STAGE_BYTES >= 4 ? 4 : 3;
+    // them load: three stages at least, four where they fit (in half the
+    // LDS for workgroups of 4 waves, which run two per CU).
+    static constexpr int LDS_BUDGET = NW == 4 ? kLdsBytes / 2 : kLdsBytes;
+    static constexpr int NSTAGE = LDS_BUDGET / STAGE_BYTES >= 4 ? 4 : 3;
     static constexpr int DMA_PER_TILE = TILE_BYTES / 1024;  // 64 lanes x 16 bytes per load
     static constexpr int DMA_PER_WAVE = (DMA_PER_TILE + NW - 1) / NW;
     static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
     static constexpr int Q_PIECES = BM * ROWB / 1024;  // 64-lane loads of the query tile
     static constexpr int Q_PER_WAVE = (Q_PIECES + NW - 1) / NW;
+    // the query tile is staged through LDS where it fits a stage's tiles;
+    // otherwise (128 rows of d = 128 over 32-key tiles) each wave loads its
+    // rows straight into registers
+    static constexpr bool Q_LDS = BM * ROWB <= 2 * BN * ROWB;
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = TAIL;        // a padding row of V^T holds ones
@@ -140,128 +134,10 @@ struct Cfg {
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
     static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads");
     static_assert(DMA_PER_TILE >= NW, "every wave loads part of each tile");
-    static_assert(BM * ROWB % 1024 == 0 && BM * ROWB <= CONST_OFF, "the query tile fits a stage's tiles");
-    static_assert(LDS_BYTES <= kLdsBytes, "LDS budget");
+    static_assert(BM * ROWB % 1024 == 0, "the query tile is whole 64-lane loads");
+    static_assert(Q_LDS || DK == D, "query rows loaded into registers have no padding chunk");
+    static_assert(LDS_BYTES <= LDS_BUDGET, "LDS budget");
 };
-
-struct Args {
-    const uint16_t* q;
-    const uint16_t* k;
-    const uint16_t* v;
-    const uint16_t* fk;
-    const uint16_t* fv;
-    uint16_t* wk;
-    uint16_t* wv;
-    uint16_t* out;
-    float* lse;
-    int B, H, Nq, Nk, q_tiles;
-    int off0, len0, off1, len1;  // fresh ranges (fresh rows: range 0's, then range 1's)
-    int sa0, sn0, sa1, sn1;      // tiles [sa, sa + sn) hold rows of fresh range 0 / 1
-    float c2;  // softmax scale * log2(e)
-    int accum;  // merge into the running (out, lse) instead of overwriting them
-    // Work partition.  A pair is one query tile of one (batch, head), pair
-    // index bh * q_tiles + qt; its sweep is T K/V tiles (T >= 1); the units
-    // (pair, tile) are counted in pair-major order, pairs * T of them.  In a
-    // partitioned launch the first G1 workgroups sweep pairs 0..G1-1 whole,
-    // one each; the units of the other pairs, [G1 * T, units), are split
-    // into G2 = gridDim.x - G1 contiguous ranges, one per further
-    // workgroup.  A workgroup walks its range as segments, one per pair it
-    // touches.  A segment over a whole sweep writes out (and lse); any other
-    // writes its normalised partial O and its LSE to slot j (the range's
-    // first segment) or G2 + j (its last) of `part`, j = the range index,
-    // for the fix-up.
-    int T;
-    int64_t units;
-    int G1;
-    float* part;
-};
-
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-
-__device__ __forceinline__ Rsrc rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcFlags);
-}
-__device__ __forceinline__ u32x4 bload(Rsrc r, uint32_t off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-}
-__device__ __forceinline__ void bstore(Rsrc r, uint32_t off, u32x4 x) {
-    __builtin_amdgcn_raw_buffer_store_b128(x, r, off, 0, 0);
-}
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes
-// land at dst + 16*l (dst must be the same in every lane).
-__device__ __forceinline__ void dma16(Rsrc r, void* dst, uint32_t off) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, off, 0, 0, 0);
-}
-
-// Wait until at most N vector-memory operations of this wave are in flight
-// (LDS and export counters left unconstrained).
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// f(integral_constant<int, I>) for I = B .. E-1, unrolled at compile time.
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
-}
-
-// Transposing LDS read (ds_read_b64_tr_b16) at byte address a + OFF, issued
-// without a wait: the caller waits with lds_wait_upto() before using the result.
-// Written as inline assembly so that the compiler does not also drain the
-// in-flight tile loads before it (it cannot tell that they target other LDS
-// bytes).
-template <int OFF>
-__device__ __forceinline__ u32x2 tr_read(uint32_t a) {
-    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
-    u32x2 r;
-    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
-    return r;
-}
-// Wait until at most N LDS reads of this wave are in flight (they complete
-// in issue order), then mark the registers of the reads that were covered.
-__device__ __forceinline__ void lds_hold_one(u32x2& r) { asm volatile("" : "+v"(r)); }
-template <int N, typename... R>
-__device__ __forceinline__ void lds_wait_upto(R&... r) {
-    static_assert(N >= 0, "lgkmcnt range");
-    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N < 15 ? N : 15));
-    (lds_hold_one(r), ...);
-}
-// Key of S^T row x (0..31) of a 32-key block: x = 16a + 8e + 4h + j is key
-// 16a + 4j + 2e + h when PERM, key x otherwise.
-template <bool PERM>
-__device__ __forceinline__ int krow(int x) {
-    if constexpr (PERM) return (x & 16) + 4 * (x & 3) + 2 * ((x >> 3) & 1) + ((x >> 2) & 1);
-    else return x;
-}
-
-__device__ __forceinline__ int xcd_remap(int pid, int total) {
-    const int per = total >> 3, rem = total & 7;
-    const int xcd = pid & 7, loc = pid >> 3;
-    return xcd * per + (xcd < rem ? xcd : rem) + loc;
-}
-
-// Two floats to a packed bf16 pair (round to nearest even): one v_cvt_pk_bf16_f32.
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    typedef float f32x2_t __attribute__((ext_vector_type(2)));
-    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
-}
-
-// x combined with its value in the other 32-lane half (lane l <-> l ^ 32);
-// the result is bit-identical in both lanes of a pair.
-__device__ __forceinline__ float halves_max(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float halves_sum(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
 
 // One segment: K/V tiles [tile0, tile0 + nt) of the sweep of pair `pair`;
 // pslot: where its partial goes, nullptr for a whole sweep.
@@ -327,22 +203,29 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     const int qrow = qt * C::BM + qb * 32 + c;
     const bool qvalid = qrow < a.Nq;
     const Rsrc ro = rsrc(out_base + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
+    // the wave's 32 query rows as B operands (lane: query c, dims
+    // 16kk+8hf..+7), held in registers for the whole sweep
+    bf16x8 qf[C::KSTEPS];
     {
         const Rsrc rq = rows_rsrc(a.q + (int64_t)b * a.Nq * a.H * D + headoff, qt * C::BM, a.Nq);
+        if constexpr (C::Q_LDS) {
 #pragma unroll
-        for (int n = 0; n < C::Q_PER_WAVE; ++n) {
-            const int ins = wave + n * C::NW;
-            if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
-                // slot p: row p / CH, logical chunk (p % CH) ^ swz(row)
-                const int p = 64 * ins + lane, r = p / C::CH;
-                dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
+            for (int n = 0; n < C::Q_PER_WAVE; ++n) {
+                const int ins = wave + n * C::NW;
+                if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
+                    // slot p: row p / CH, logical chunk (p % CH) ^ swz(row)
+                    const int p = 64 * ins + lane, r = p / C::CH;
+                    dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
+                }
             }
+        } else {
+            // straight into registers, issued before the tile loads (the
+            // prologue's wait for tile 0 covers them)
+#pragma unroll
+            for (int kk = 0; kk < C::KSTEPS; ++kk)
+                qf[kk] = __builtin_bit_cast(bf16x8, bload(rq, (uint32_t)(qb * 32 + c) * rowb + 32 * kk + 16 * hf));
         }
     }
-    // the wave's 32 query rows as B operands (lane: query c, dims
-    // 16kk+8hf..+7), read from LDS after the prologue and held in registers
-    // for the whole sweep
-    bf16x8 qf[C::KSTEPS];
     // Tile loads: load n of this wave fills LDS chunks 64*ins .. 64*ins+63
     // of a tile (ins = wave + n*NW); lane l's chunk p = 64*ins + l holds
     // row p / CH, logical chunk (p % CH) ^ swizzle(row).  dma_off is its
@@ -720,10 +603,18 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
+    if constexpr (C::Q_LDS) {
 #pragma unroll
-    for (int kk = 0; kk < C::KSTEPS; ++kk) {
-        const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
-        qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
+        for (int kk = 0; kk < C::KSTEPS; ++kk) {
+            const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
+            qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
+        }
+    } else {
+        // the compiler waits here for the register loads (all older than
+        // the tile loads), so that no path into the loop leaves them
+        // outstanding
+#pragma unroll
+        for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" : "+v"(qf[kk]));
     }
     if (ntiles > 0) {
         qk(0, sA);
@@ -856,7 +747,6 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
             m_ref = M;
         }
     }
-    static_assert(KS > 1, "key-split waves merge into those of split 0");
     if (kh != 0) {
         if constexpr (PATCH) copy_rest();
         return;
@@ -985,8 +875,11 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 // whole), or a partitioned launch (PARTS = true, see Args).  Workgroup ids
 // are remapped per group (whole sweeps, cut ranges) so that neighbouring
 // pairs share an XCD; G1 is a multiple of 8, so both groups start on XCD 0.
+// Workgroups of 4 waves (one per SIMD) are built to run two per CU: each
+// wave is then held to 256 registers, so that every SIMD interleaves two
+// waves of independent workgroups, which no barrier keeps in step.
 template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS>
-__global__ __launch_bounds__(64 * QB * KS) void attn_bf16_kernel(Args a) {
+__global__ __launch_bounds__(64 * QB * KS, QB * KS == 4 ? 2 : 1) void attn_bf16_kernel(Args a) {
     using C = Cfg<D, QB, KS, KW>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
     if constexpr (!PARTS) {
@@ -1172,6 +1065,36 @@ __global__ __launch_bounds__(256) void fixup_kernel(FixArgs a) {
     if (a.lse && dg == 0) a.lse[lidx] = L_out;
 }
 
+// The fix-up launch after a partitioned sweep of 128-row query tiles, each
+// sweep T K/V tiles long: merges the partials of the cut sweeps.
+template <int D>
+hipError_t launch_fixup(const AttnParams& p, int q_tiles, int T, hipStream_t s) {
+    constexpr int BM = kPartSlotRows;
+    if (p.parts < 2) return hipSuccess;
+    const int64_t pairs = (int64_t)q_tiles * p.H * p.B;
+    FixArgs f;
+    f.out = (uint16_t*)p.out;
+    f.lse = p.lse;
+    f.part = p.part;
+    f.B = p.B;
+    f.H = p.H;
+    f.Nq = p.Nq;
+    f.q_tiles = q_tiles;
+    f.T = T;
+    f.G2 = (int)p.parts;
+    f.base = p.whole * T;
+    f.rem = pairs * T - f.base;
+    const int64_t cut = pairs - p.whole;  // query tiles in the cut ranges
+    f.s_al = p.parts % cut == 0 ? (int)(p.parts / cut) : 0;
+    f.accum = p.accum;
+    // one part per cut query tile, or sweeps of one tile: every part swept
+    // its query tile whole and wrote it, nothing to merge
+    if (f.s_al == 1 || T == 1) return hipSuccess;
+    const int64_t gx = f.s_al > 0 ? cut : p.parts - 1;
+    hipLaunchKernelGGL((fixup_kernel<D, BM>), dim3((unsigned)gx, BM / kFixRows), dim3(256), 0, s, f);
+    return hipGetLastError();
+}
+
 template <int D, int QB, int KS, int KW, bool PATCH>
 hipError_t launch(const AttnParams& p, hipStream_t s) {
     using C = Cfg<D, QB, KS, KW>;
@@ -1220,29 +1143,8 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
         hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, true>), dim3((unsigned)(p.whole + p.parts)),
                            dim3(C::THREADS), 0, s, a);
         hipError_t e = hipGetLastError();
-        if (e != hipSuccess || p.parts < 2) return e;
-        // merge the partials of the cut sweeps
-        FixArgs f;
-        f.out = a.out;
-        f.lse = a.lse;
-        f.part = a.part;
-        f.B = p.B;
-        f.H = p.H;
-        f.Nq = p.Nq;
-        f.q_tiles = a.q_tiles;
-        f.T = a.T;
-        f.G2 = (int)p.parts;
-        f.base = p.whole * a.T;
-        f.rem = a.units - f.base;
-        const int64_t cut = pairs - p.whole;  // query tiles in the cut ranges
-        f.s_al = p.parts % cut == 0 ? (int)(p.parts / cut) : 0;
-        f.accum = p.accum;
-        // one part per cut query tile, or sweeps of one tile: every part
-        // swept its query tile whole and wrote it, nothing to merge
-        if (f.s_al == 1 || a.T == 1) return hipSuccess;
-        const int64_t gx = f.s_al > 0 ? cut : p.parts - 1;
-        hipLaunchKernelGGL((fixup_kernel<D, C::BM>), dim3((unsigned)gx, C::BM / kFixRows), dim3(256), 0, s, f);
-        return hipGetLastError();
+        if (e != hipSuccess) return e;
+        return launch_fixup<D>(p, a.q_tiles, a.T, s);
     }
 }
 
@@ -1269,8 +1171,25 @@ int forced_shape() {
     return 0;
 }
 
+// XDIT_ATTN_KERNEL selects the decomposition: "w64" (64 query rows per
+// wave, attn_w64.hip, head dim 128), "o2" (workgroups of 4 waves, two per
+// CU), or the 8-wave workgroups of this file ("w32", the default).
+static int attn_kernel_choice() {
+    const char* e = getenv("XDIT_ATTN_KERNEL");
+    if (e != nullptr && strcmp(e, "w64") == 0) return 64;
+    if (e != nullptr && strcmp(e, "o2") == 0) return 2;
+    return 32;
+}
+
 template <int D, bool PATCH>
 hipError_t dispatch(const AttnParams& p, hipStream_t s) {
+    if (attn_kernel_choice() == 2) {
+        // 128 rows x 32-key tiles at d = 128; 64 rows (2 blocks x 2 key
+        // splits of a 64-key tile) at d <= 72, whose partitioned launches
+        // keep the 8-wave shape (128-row slots)
+        if constexpr (D > 96) return launch<D, 4, 1, 32, PATCH>(p, s);
+        else if (p.parts <= 0) return launch<D, 2, 2, 32, PATCH>(p, s);
+    }
     if constexpr (D > 96) {
         return launch<D, 4, 2, 32, PATCH>(p, s);
     } else {
@@ -1289,8 +1208,18 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
 
 }  // namespace
 
+hipError_t launch_attn_fixup(const AttnParams& p, int q_tiles, int T, hipStream_t s) {
+    switch (p.D) {
+        case 64: return launch_fixup<64>(p, q_tiles, T, s);
+        case 72: return launch_fixup<72>(p, q_tiles, T, s);
+        case 128: return launch_fixup<128>(p, q_tiles, T, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_attn_bf16(const AttnParams& p, hipStream_t s) {
     const bool patch = p.fresh_k != nullptr;
+    if (p.D == 128 && attn_kernel_choice() == 64) return launch_attn_w64(p, s);
     switch (p.D) {
         case 64: return patch ? dispatch<64, true>(p, s) : dispatch<64, false>(p, s);
         case 72: return patch ? dispatch<72, true>(p, s) : dispatch<72, false>(p, s);

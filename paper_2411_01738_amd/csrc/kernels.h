@@ -62,6 +62,13 @@ constexpr int kPartSlotRows = 128;  // query rows of a partitioned launch's tile
 constexpr int kMaxSweepParts = 17;  // most partition ranges one sweep may meet
 
 hipError_t launch_attn_bf16(const AttnParams& p, hipStream_t s);
+// The second launch of a partitioned bf16 attention (128-row query tiles,
+// sweeps of T K/V tiles): merges the partials of the cut sweeps into out
+// and lse.
+hipError_t launch_attn_fixup(const AttnParams& p, int q_tiles, int T, hipStream_t s);
+// bf16 attention with 64 query rows per wave and one wave per SIMD (head
+// dim 128); hipErrorNotSupported for shapes it does not take.
+hipError_t launch_attn_w64(const AttnParams& p, hipStream_t s);
 hipError_t launch_attn_f32(const AttnParams& p, hipStream_t s);
 hipError_t launch_merge_bf16(const MergeParams& p, hipStream_t s);
 hipError_t launch_merge_f32(const MergeParams& p, hipStream_t s);

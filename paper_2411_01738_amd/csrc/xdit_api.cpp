@@ -669,7 +669,9 @@ struct GemmPlan {
 
 std::mutex g_gemm_mutex;
 std::map<int, hipblasLtHandle_t> g_handles;
-std::map<std::tuple<int, int64_t, int64_t, int64_t>, GemmPlan> g_plans;
+// plans by (device, M, N, K, batch)
+std::map<std::tuple<int, int64_t, int64_t, int64_t, int>, GemmPlan> g_plans;
+constexpr int kNoAlgorithm = 1;  // gemm_bf16: hipBLASLt offers no algorithm for the shape
 
 int blas_status(hipblasStatus_t st, const char* what) {
     if (st != HIPBLAS_STATUS_SUCCESS) return fail(XDIT_ERR_HIP, "%s: hipBLASLt status %d", what, (int)st);
@@ -678,8 +680,13 @@ int blas_status(hipblasStatus_t st, const char* what) {
 
 // Row-major C[M, N] = A[M, K] B[K, N], all bf16 and contiguous.  In
 // hipBLASLt's column-major terms that is C^T (N x M) = B^T (N x K) A^T (K x M),
-// where B^T and A^T are the row-major buffers read as column-major.
-int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K) {
+// where B^T and A^T are the row-major buffers read as column-major.  With
+// batch > 1: C_i = A B_i for i < batch, the B_i and the C_i consecutive
+// (one strided-batched launch; A is shared, batch stride 0).  Returns
+// kNoAlgorithm, with no error set and nothing launched, when hipBLASLt has
+// no algorithm for the shape.
+int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,
+              int batch = 1) {
     if (M == 0 || N == 0) return XDIT_OK;
     int dev = 0;
     XDIT_TRY(hip_status(hipGetDevice(&dev), fn));
@@ -691,7 +698,7 @@ int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, 
         hit = g_handles.emplace(dev, h).first;
     }
     const hipblasLtHandle_t handle = hit->second;
-    const auto key = std::make_tuple(dev, M, N, K);
+    const auto key = std::make_tuple(dev, M, N, K, batch);
     auto pit = g_plans.find(key);
     if (pit == g_plans.end()) {
         GemmPlan pl;
@@ -705,6 +712,23 @@ int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, 
         XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.la, HIP_R_16BF, N, K, N), "hipblasLtMatrixLayoutCreate"));
         XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.lb, HIP_R_16BF, K, M, K), "hipblasLtMatrixLayoutCreate"));
         XDIT_TRY(blas_status(hipblasLtMatrixLayoutCreate(&pl.ld, HIP_R_16BF, N, M, N), "hipblasLtMatrixLayoutCreate"));
+        if (batch > 1) {
+            const int32_t bc = batch;
+            const int64_t sb = N * K, sa = 0, sc = N * M;
+            for (hipblasLtMatrixLayout_t l : {pl.la, pl.lb, pl.ld})
+                XDIT_TRY(blas_status(hipblasLtMatrixLayoutSetAttribute(l, HIPBLASLT_MATRIX_LAYOUT_BATCH_COUNT, &bc,
+                                                                       sizeof(bc)),
+                                     "hipblasLtMatrixLayoutSetAttribute"));
+            XDIT_TRY(blas_status(hipblasLtMatrixLayoutSetAttribute(pl.la, HIPBLASLT_MATRIX_LAYOUT_STRIDED_BATCH_OFFSET,
+                                                                   &sb, sizeof(sb)),
+                                 "hipblasLtMatrixLayoutSetAttribute"));
+            XDIT_TRY(blas_status(hipblasLtMatrixLayoutSetAttribute(pl.lb, HIPBLASLT_MATRIX_LAYOUT_STRIDED_BATCH_OFFSET,
+                                                                   &sa, sizeof(sa)),
+                                 "hipblasLtMatrixLayoutSetAttribute"));
+            XDIT_TRY(blas_status(hipblasLtMatrixLayoutSetAttribute(pl.ld, HIPBLASLT_MATRIX_LAYOUT_STRIDED_BATCH_OFFSET,
+                                                                   &sc, sizeof(sc)),
+                                 "hipblasLtMatrixLayoutSetAttribute"));
+        }
         hipblasLtMatmulPreference_t pref = nullptr;
         XDIT_TRY(blas_status(hipblasLtMatmulPreferenceCreate(&pref), "hipblasLtMatmulPreferenceCreate"));
         uint64_t ws = 0;
@@ -715,6 +739,13 @@ int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, 
         const hipblasStatus_t st = hipblasLtMatmulAlgoGetHeuristic(handle, pl.desc, pl.la, pl.lb, pl.ld, pl.ld, pref,
                                                                    kCands, res, &nres);
         hipblasLtMatmulPreferenceDestroy(pref);
+        if (batch > 1 && (st != HIPBLAS_STATUS_SUCCESS || nres < 1)) {
+            hipblasLtMatrixLayoutDestroy(pl.la);
+            hipblasLtMatrixLayoutDestroy(pl.lb);
+            hipblasLtMatrixLayoutDestroy(pl.ld);
+            hipblasLtMatmulDescDestroy(pl.desc);
+            return kNoAlgorithm;
+        }
         XDIT_TRY(blas_status(st, "hipblasLtMatmulAlgoGetHeuristic"));
         if (nres < 1)
             return fail(XDIT_ERR_HIP, "%s: hipBLASLt has no algorithm for a %lld x %lld x %lld bf16 GEMM", fn,
@@ -753,6 +784,19 @@ int gemm_bf16(const char* fn, const void* A, const void* B, void* C, int64_t M, 
                 }
             (void)hipEventDestroy(e0);
             (void)hipEventDestroy(e1);
+        }
+        if (batch > 1) {
+            // a batched plan is kept only if its algorithm runs (a shared
+            // operand with batch stride 0 is not taken by every kernel)
+            const float one = 1.f, zero = 0.f;
+            if (hipblasLtMatmul(handle, pl.desc, &one, B, pl.la, A, pl.lb, &zero, C, pl.ld, C, pl.ld, &pl.algo,
+                                nullptr, 0, g_stream) != HIPBLAS_STATUS_SUCCESS) {
+                hipblasLtMatrixLayoutDestroy(pl.la);
+                hipblasLtMatrixLayoutDestroy(pl.lb);
+                hipblasLtMatrixLayoutDestroy(pl.ld);
+                hipblasLtMatmulDescDestroy(pl.desc);
+                return kNoAlgorithm;
+            }
         }
         pit = g_plans.emplace(key, pl).first;
     }
@@ -793,9 +837,22 @@ extern "C" int xdit_stage_step(const void* x, const void* wq, const void* wk, co
         for (int j = 0; j < i; ++j) XDIT_TRY(check_no_overlap(*outs[i], *outs[j]));
     }
     if (M == 0 || heads == 0) return XDIT_OK;
-    XDIT_TRY(gemm_bf16(fn, x, wq, q, M, HD, hidden));
-    XDIT_TRY(gemm_bf16(fn, x, wk, k, M, HD, hidden));
-    XDIT_TRY(gemm_bf16(fn, x, wv, v, M, HD, hidden));
+    // The three projections as one strided-batched GEMM when the weights
+    // are consecutive [3, C, H*d] and q, k, v consecutive [3, B, L, H, d];
+    // otherwise (or if hipBLASLt has no batched algorithm) three GEMMs.
+    const int64_t wbytes = hidden * HD * 2, obytes = M * HD * 2;
+    const char *cq = (const char*)q, *cwq = (const char*)wq;
+    int rc = kNoAlgorithm;
+    if ((const char*)wk == cwq + wbytes && (const char*)wv == cwq + 2 * wbytes && (const char*)k == cq + obytes &&
+        (const char*)v == cq + 2 * obytes)
+        rc = gemm_bf16(fn, x, wq, q, M, HD, hidden, 3);
+    if (rc == kNoAlgorithm) {
+        XDIT_TRY(gemm_bf16(fn, x, wq, q, M, HD, hidden));
+        XDIT_TRY(gemm_bf16(fn, x, wk, k, M, HD, hidden));
+        XDIT_TRY(gemm_bf16(fn, x, wv, v, M, HD, hidden));
+    } else {
+        XDIT_TRY(rc);
+    }
     XDIT_TRY(patch_ranges_impl(fn, q, patch_len, kv_buf, 1, &patch_off, &patch_len, k, v, o, nullptr, batch,
                                seq_len, heads, head_dim, dtype));
     return gemm_bf16(fn, o, wo, y, M, hidden, HD);

@@ -59,14 +59,19 @@ class HotPath:
         self.stage = None
         if w.hidden:
             C = w.hidden
-            self.stage = {"w": [up(t.extra[n]) for n in ("wq", "wk", "wv", "wo")],
+            # wq, wk, wv in one [3, C, H*d] tensor and q, k, v of a step in one
+            # [3, B, L, H, d] tensor: the library then runs the three
+            # projections as one batched GEMM
+            wqkv = up(np.stack([t.extra[n] for n in ("wq", "wk", "wv")]))
+            self.stage = {"w": [wqkv[0], wqkv[1], wqkv[2], up(t.extra["wo"])],
                           "x": [], "y": [], "qkvo": []}
             for ranges, qrows in self.calls:
                 (off, ln), = ranges
                 self.stage["x"].append(up(t.extra["x"][:, off:off + ln]))
                 self.stage["y"].append(torch.empty((B, ln, C), device=device, dtype=dt))
-                self.stage["qkvo"].append([torch.empty((B, ln, H, d), device=device, dtype=dt)
-                                           for _ in range(4)])
+                qkv = torch.empty((3, B, ln, H, d), device=device, dtype=dt)
+                self.stage["qkvo"].append([qkv[0], qkv[1], qkv[2],
+                                           torch.empty((B, ln, H, d), device=device, dtype=dt)])
         self.sp_q = self.sp_out = self.sp_lse = None
         self.chunk_k, self.chunk_v, self.chunk_out, self.chunk_lse = [], [], [], []
         if w.sp_chunks:

@@ -56,15 +56,26 @@ CASES = [(2, 96, 320, 2, 72, 160, 64), (1, 130, 300, 3, 64, 192, 170),
          (2, 64, 256, 2, 128, 256, 0), (1, 1, 128, 2, 64, 64, 127), (1, 200, 200, 1, 72, 72, 0)]
 
 
+@pytest.mark.parametrize("packed", [False, True], ids=["separate", "packed"])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_L{}_N{}_H{}_d{}_C{}_off{}".format(*c))
-def test_stage_step(case):
+def test_stage_step(case, packed):
+    """packed: wq, wk, wv consecutive in one [3, C, H*d] tensor and q, k, v
+    in one [3, B, L, H, d] tensor, the layout the library projects with one
+    batched GEMM; separate: five independent allocations."""
     torch = torch_mod()
     B, L, N, H, d, C, off = case
     x, (wq, wk, wv), wo, kv = _inputs(B, L, N, H, d, C, 700 + L)
-    print(f"[stage] {case}", flush=True)
-    g = {n: to_gpu(a, "bf16") for n, a in (("x", x), ("wq", wq), ("wk", wk), ("wv", wv), ("wo", wo),
-                                           ("kv", kv))}
-    q, k, v, o = (torch.empty((B, L, H, d), device="cuda", dtype=torch.bfloat16) for _ in range(4))
+    print(f"[stage] {case} packed={packed}", flush=True)
+    g = {n: to_gpu(a, "bf16") for n, a in (("x", x), ("wo", wo), ("kv", kv))}
+    if packed:
+        wqkv = to_gpu(np.stack([wq, wk, wv]), "bf16")
+        g["wq"], g["wk"], g["wv"] = wqkv[0], wqkv[1], wqkv[2]
+        qkv = torch.empty((3, B, L, H, d), device="cuda", dtype=torch.bfloat16)
+        q, k, v = qkv[0], qkv[1], qkv[2]
+        o = torch.empty((B, L, H, d), device="cuda", dtype=torch.bfloat16)
+    else:
+        g.update({n: to_gpu(a, "bf16") for n, a in (("wq", wq), ("wk", wk), ("wv", wv))})
+        q, k, v, o = (torch.empty((B, L, H, d), device="cuda", dtype=torch.bfloat16) for _ in range(4))
     y = torch.empty((B, L, C), device="cuda", dtype=torch.bfloat16)
     xdit_stage_step(g["x"], g["wq"], g["wk"], g["wv"], g["wo"], g["kv"], off, q, k, v, o, y)
     torch.cuda.synchronize()
