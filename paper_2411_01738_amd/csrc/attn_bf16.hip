@@ -1173,17 +1173,20 @@ int forced_shape() {
 
 // XDIT_ATTN_KERNEL selects the decomposition: "w64" (64 query rows per
 // wave, attn_w64.hip, head dim 128), "o2" (workgroups of 4 waves, two per
-// CU), or the 8-wave workgroups of this file ("w32", the default).
-static int attn_kernel_choice() {
+// CU) or "w32" (the 8-wave workgroups of this file).  Unset: o2 at d = 128
+// (the Flux chunk step measured 221 vs 228-236 us), w32 at d <= 72 (o2's
+// 64-row, 64-key shape measured 10-18 % slower there).
+static int attn_kernel_choice(int D) {
     const char* e = getenv("XDIT_ATTN_KERNEL");
     if (e != nullptr && strcmp(e, "w64") == 0) return 64;
     if (e != nullptr && strcmp(e, "o2") == 0) return 2;
-    return 32;
+    if (e != nullptr && strcmp(e, "w32") == 0) return 32;
+    return D > 96 ? 2 : 32;
 }
 
 template <int D, bool PATCH>
 hipError_t dispatch(const AttnParams& p, hipStream_t s) {
-    if (attn_kernel_choice() == 2) {
+    if (attn_kernel_choice(D) == 2) {
         // 128 rows x 32-key tiles at d = 128; 64 rows (2 blocks x 2 key
         // splits of a 64-key tile) at d <= 72, whose partitioned launches
         // keep the 8-wave shape (128-row slots)
@@ -1219,7 +1222,7 @@ hipError_t launch_attn_fixup(const AttnParams& p, int q_tiles, int T, hipStream_
 
 hipError_t launch_attn_bf16(const AttnParams& p, hipStream_t s) {
     const bool patch = p.fresh_k != nullptr;
-    if (p.D == 128 && attn_kernel_choice() == 64) return launch_attn_w64(p, s);
+    if (p.D == 128 && attn_kernel_choice(p.D) == 64) return launch_attn_w64(p, s);
     switch (p.D) {
         case 64: return patch ? dispatch<64, true>(p, s) : dispatch<64, false>(p, s);
         case 72: return patch ? dispatch<72, true>(p, s) : dispatch<72, false>(p, s);

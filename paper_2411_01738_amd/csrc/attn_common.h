@@ -98,6 +98,21 @@ __device__ __forceinline__ u32x2 tr_read(uint32_t a) {
     asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
     return r;
 }
+// A 16-byte LDS read at byte address a + OFF, issued without a wait (the
+// caller waits for it by lgkmcnt).
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_b128(uint32_t a) {
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+    u32x4 r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
+    return r;
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait_v4(u32x4& r) {
+    static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N));
+    asm volatile("" : "+v"(r));
+}
 // Wait until at most N LDS reads of this wave are in flight (they complete
 // in issue order), then mark the registers of the reads that were covered.
 __device__ __forceinline__ void lds_hold_one(u32x2& r) { asm volatile("" : "+v"(r)); }

@@ -98,14 +98,8 @@ __device__ __forceinline__ int krow128(int x) {
 }
 
 // LDS reads issued without a wait (the caller waits with lgkm_wait): a
-// 16-byte read and a transposing 8-byte read at byte address a + OFF.
-template <int OFF>
-__device__ __forceinline__ u32x4 lds_b128(uint32_t a) {
-    static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
-    u32x4 r;
-    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
-    return r;
-}
+// transposing 8-byte read at byte address a + OFF (lds_b128 of
+// attn_common.h is the 16-byte one).
 // the same into AGPRs (the query operands, read only by inline assembly)
 __device__ __forceinline__ u32x4 lds_b128_agpr(uint32_t a) {
     u32x4 r;
