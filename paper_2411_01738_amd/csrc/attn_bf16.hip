@@ -102,13 +102,21 @@ struct Cfg {
     static constexpr bool E_SPLIT = CH == 8 || CH == 16;
     static constexpr bool SWIZZLED = CH == 8 || CH == 16;  // swz is not identically zero
     static constexpr int TILE_BYTES = BN * ROWB;     // one K or V tile
-    static constexpr int CONST_OFF = 2 * TILE_BYTES;  // 16 zero bytes, then the ones chunk
-    static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 32;
+    // LDS layout: the K regions of the stages, then their V regions; a
+    // region is one tile, then 16 zero bytes and the ones chunk (read by
+    // the lanes of padding dims).  With K and V apart, every operand read
+    // of a stage known at compile time is one per-lane base register plus
+    // an immediate offset (all below 64 KiB), with no address arithmetic
+    // per read.
+    static constexpr int REGION = TILE_BYTES + 32;
+    static constexpr int CONST_OFF = TILE_BYTES;      // within a region
+    static constexpr int STAGE_BYTES = 2 * REGION;
     // Iteration t reads V of tile t and K of tile t+1 while the tiles after
     // them load: three stages at least, four where they fit (in half the
     // LDS for workgroups of 4 waves, which run two per CU).
     static constexpr int LDS_BUDGET = NW == 4 ? kLdsBytes / 2 : kLdsBytes;
     static constexpr int NSTAGE = LDS_BUDGET / STAGE_BYTES >= 4 ? 4 : 3;
+    static constexpr int VBASE = NSTAGE * REGION;     // the first V region
     static constexpr int DMA_PER_TILE = TILE_BYTES / 1024;  // 64 lanes x 16 bytes per load
     static constexpr int DMA_PER_WAVE = (DMA_PER_TILE + NW - 1) / NW;
     static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
@@ -117,7 +125,7 @@ struct Cfg {
     // the query tile is staged through LDS where it fits a stage's tiles;
     // otherwise (128 rows of d = 128 over 32-key tiles) each wave loads its
     // rows straight into registers
-    static constexpr bool Q_LDS = BM * ROWB <= 2 * BN * ROWB;
+    static constexpr bool Q_LDS = BM * ROWB <= TILE_BYTES;  // in the K region of stage NSTAGE-1
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = TAIL;        // a padding row of V^T holds ones
@@ -137,6 +145,7 @@ struct Cfg {
     static_assert(BM * ROWB % 1024 == 0, "the query tile is whole 64-lane loads");
     static_assert(Q_LDS || DK == D, "query rows loaded into registers have no padding chunk");
     static_assert(LDS_BYTES <= LDS_BUDGET, "LDS budget");
+    static_assert(NSTAGE == 4, "the main loop is unrolled over four stages");
 };
 
 // One segment: K/V tiles [tile0, tile0 + nt) of the sweep of pair `pair`;
@@ -184,14 +193,16 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         return rsrc(base + (int64_t)row0 * a.H * D, rows > row0 ? (uint32_t)(rows - row0) * rowb - headb : 0u);
     };
 
-    auto stage = [&](int s) -> unsigned char* { return lds + s * C::STAGE_BYTES; };
+    // K and V regions of stage s
+    auto kreg = [&](int s) -> unsigned char* { return lds + s * C::REGION; };
+    auto vreg = [&](int s) -> unsigned char* { return lds + C::VBASE + s * C::REGION; };
     const uint32_t lds_u32 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)lds;
 
-    // Constant chunks of every stage: 16 zero bytes, then bf16 {1, 0, 0, 0,
-    // 0, 0, 0, 0} (the ones entry of the row-sum row of V^T).
-    if (tid < 2 * NST) {
-        const int s = tid >> 1;
-        *(u32x4*)(stage(s) + C::CONST_OFF + 16 * (tid & 1)) =
+    // Constant chunks of every region: 16 zero bytes, then bf16 {1, 0, 0,
+    // 0, 0, 0, 0, 0} (the ones entry of the row-sum row of V^T).
+    if (tid < 4 * NST) {
+        const int rg = tid >> 1;  // regions: K of the stages, then V
+        *(u32x4*)(lds + rg * C::REGION + C::CONST_OFF + 16 * (tid & 1)) =
             (tid & 1) ? u32x4{0x3f80u, 0, 0, 0} : u32x4{0, 0, 0, 0};
     }
 
@@ -215,7 +226,7 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
                 if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
                     // slot p: row p / CH, logical chunk (p % CH) ^ swz(row)
                     const int p = 64 * ins + lane, r = p / C::CH;
-                    dma16(rq, stage(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
+                    dma16(rq, kreg(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
                 }
             }
         } else {
@@ -244,8 +255,8 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     // their sources on the long one.
     auto load_tile = [&](int t, int s) {
         const int gt = tb + t, lo = gt * BN;
-        unsigned char* kdst = stage(s);
-        unsigned char* vdst = stage(s) + C::TILE_BYTES;
+        unsigned char* kdst = kreg(s);
+        unsigned char* vdst = vreg(s);
         auto issue = [&](Rsrc rk, Rsrc rv) {
 #pragma unroll
             for (int n = 0; n < C::DMA_PER_WAVE; ++n) {
@@ -316,12 +327,20 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     //  (see pv).  Padding dims read the constant chunks (ones for dim d,
     //  zeros after it).
     const int kw0 = kh * KW;  // this wave's first key within a tile
+    // LDS byte addresses within stage 0's K region (a stage adds a multiple
+    // of REGION); kpad[kb]: the padded last k-step of d = 72, whose lanes of
+    // the zero chunk read it in every 32-key block
     uint32_t kaddr[C::KSTEPS];
 #pragma unroll
     for (int kk = 0; kk < C::KSTEPS; ++kk) {
         const int r = kw0 + krow<C::PERM>(c), lc = 2 * kk + hf;
-        kaddr[kk] = lc < C::CH ? r * C::ROWB + 16 * (lc ^ C::swz(r)) : C::CONST_OFF;
+        kaddr[kk] = lds_u32 + (lc < C::CH ? r * C::ROWB + 16 * (lc ^ C::swz(r)) : C::CONST_OFF);
     }
+    constexpr bool KPAD = C::CH % 2 != 0;  // the last k-step's second half is the zero chunk
+    uint32_t kpad[NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+        kpad[kb] = kaddr[C::KSTEPS - 1] + (KPAD && hf ? 0u : (uint32_t)(32 * kb * C::ROWB));
     const int gi = lane & 15, grp = lane >> 4;
     const int vkey0 = kw0 + krow<C::PERM>(4 * hf + (gi >> 2));
     constexpr int NE = C::E_SPLIT ? 2 : 1;
@@ -331,16 +350,27 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         const int dim = 32 * db + 16 * (grp & 1) + 4 * (gi & 3);
         for (int e = 0; e < NE; ++e) {
             const int r = vkey0 + C::E_ROWS * e;
-            vaddr[db][e] = C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7);
+            vaddr[db][e] = lds_u32 + C::VBASE + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7);
         }
     }
-    uint32_t vtaddr = 0;  // tail: k-step pair 0, half step e = 0
+    // tail: vtad[p][e] = read address of k-step pair p, half step e (in
+    // stage 0's V region); lanes of padding dims read the constant chunk
+    // in every step
+    constexpr int NPT = C::TAIL ? NKS / 2 : 0;
+    uint32_t vtad[NPT > 0 ? NPT : 1][2] = {};
     if constexpr (C::TAIL) {
         static_assert(!C::E_SPLIT, "tail reads step by E_ROWS rows between half k-steps");
         const int dim = C::TB + 4 * (gi & 3);
         const int r = kw0 + krow<C::PERM>(4 * (grp >> 1) + (gi >> 2)) + 16 * (grp & 1);
-        vtaddr = dim < D ? C::TILE_BYTES + r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7)
-                         : (dim == D ? C::CONST_OFF + 16 : C::CONST_OFF);
+        const bool cst = dim >= D;
+        const uint32_t base = lds_u32 + C::VBASE +
+                              (!cst ? r * C::ROWB + 16 * ((dim >> 3) ^ C::swz(r)) + 2 * (dim & 7)
+                                    : (dim == D ? C::CONST_OFF + 16 : C::CONST_OFF));
+#pragma unroll
+        for (int pp = 0; pp < NPT; ++pp)
+#pragma unroll
+            for (int e = 0; e < 2; ++e)
+                vtad[pp][e] = base + (cst ? 0u : (uint32_t)((32 * pp + C::E_ROWS * e) * C::ROWB));
     }
 
     f32x16 oacc[C::DBLK];
@@ -357,24 +387,29 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 
     // S^T of tile t for this wave's KW keys x 32 queries: s[kb][i] = score of
     // key kw0 + 32kb + krow(8(i/4) + 4hf + (i%4)) of the tile against query c.
-    auto qk = [&](int t, f32x16 (&s)[NKB]) {
-        const unsigned char* st = stage(t % NST);
+    // The stage of tile t is S when S >= 0 (a compile-time constant: its
+    // offset is part of every read's immediate), else t % NST.
+    auto qk = [&](int t, f32x16 (&s)[NKB], auto stage_c) {
+        constexpr int S = decltype(stage_c)::value;
+        constexpr uint32_t SI = S >= 0 ? (uint32_t)(S * C::REGION) : 0u;
+        const uint32_t so = S >= 0 ? 0u : (uint32_t)((t % NST) * C::REGION);
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) s[kb] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk)
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
-                bf16x8 ka;
+                uint32_t ad;
                 if (!C::SWIZZLED && 2 * kk + 1 < C::CH) {
                     // unswizzled rows: chunk 2kk + hf sits 32kk bytes past
                     // chunk hf, an immediate offset of one address
-                    ka = *(const bf16x8*)(st + kaddr[0] + 32 * kk + 32 * kb * C::ROWB);
+                    ad = kaddr[0] + so + (SI + 32 * kk + 32 * kb * C::ROWB);
+                } else if (KPAD && kk == C::KSTEPS - 1) {
+                    ad = kpad[kb] + so + SI;
                 } else {
-                    uint32_t ad = kaddr[kk] + 32 * kb * C::ROWB;
-                    if (2 * kk + 1 >= C::CH && kb > 0 && kaddr[kk] == (uint32_t)C::CONST_OFF) ad = C::CONST_OFF;
-                    ka = *(const bf16x8*)(st + ad);
+                    ad = kaddr[kk] + so + (SI + 32 * kb * C::ROWB);
                 }
+                const bf16x8 ka = lds_ld<bf16x8>(ad);
                 s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s[kb], 0, 0, 0);
             }
     };
@@ -457,7 +492,6 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     // full blocks in vr, the tail (one operand per pair of k-steps) in vt.
     // They are issued in the order pv consumes them: per k-step its full
     // blocks, then after each odd step the tail operand of the pair.
-    constexpr int NPT = C::TAIL ? NKS / 2 : 0;
     // reads of k-step j; reads issued after those of step ks's full blocks
     // (tail = false) or after its tail operand (tail = true)
     constexpr auto vt_reads = [](int j) { return 2 * C::DBLK + (C::TAIL && (j & 1) ? 2 : 0); };
@@ -466,30 +500,28 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         for (int j = ks + 1; j < NKS; ++j) n += vt_reads(j);
         return n + (!tail && C::TAIL && (ks & 1) ? 2 : 0);
     };
-    auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2], u32x2 (&vt)[NPT > 0 ? NPT : 1][2]) {
-        const uint32_t vst = lds_u32 + (uint32_t)((t % NST) * C::STAGE_BYTES);
-        // lanes of padding dims keep reading the constant chunk
-        const bool cst = vtaddr >= (uint32_t)C::CONST_OFF;
+    auto read_vt = [&](int t, u32x2 (&vr)[NKS][C::DBLK][2], u32x2 (&vt)[NPT > 0 ? NPT : 1][2], auto stage_c) {
+        constexpr int S = decltype(stage_c)::value;
+        constexpr int SI = S >= 0 ? S * C::REGION : 0;
+        const uint32_t so = S >= 0 ? 0u : (uint32_t)((t % NST) * C::REGION);
         static_for<0, NKS>([&](auto ksc) {
             constexpr int ks = decltype(ksc)::value;
             static_for<0, C::DBLK>([&](auto dbc) {
                 constexpr int db = decltype(dbc)::value;
                 if constexpr (C::E_SPLIT) {
-                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][0]);
-                    vr[ks][db][1] = tr_read<16 * ks * C::ROWB>(vst + vaddr[db][NE - 1]);
+                    vr[ks][db][0] = tr_read<SI + 16 * ks * C::ROWB>(vaddr[db][0] + so);
+                    vr[ks][db][1] = tr_read<SI + 16 * ks * C::ROWB>(vaddr[db][NE - 1] + so);
                 } else {
                     // unswizzled rows: block db's dims sit 64db bytes past block 0's
                     static_assert(!C::SWIZZLED, "one address for all blocks");
-                    vr[ks][db][0] = tr_read<16 * ks * C::ROWB + 64 * db>(vst + vaddr[0][0]);
-                    vr[ks][db][1] = tr_read<(16 * ks + C::E_ROWS) * C::ROWB + 64 * db>(vst + vaddr[0][0]);
+                    vr[ks][db][0] = tr_read<SI + 16 * ks * C::ROWB + 64 * db>(vaddr[0][0] + so);
+                    vr[ks][db][1] = tr_read<SI + (16 * ks + C::E_ROWS) * C::ROWB + 64 * db>(vaddr[0][0] + so);
                 }
             });
             if constexpr (C::TAIL && (ks & 1)) {
                 constexpr int pp = ks >> 1;
-                const uint32_t a0 = vst + vtaddr + (cst ? 0u : (uint32_t)(32 * pp * C::ROWB));
-                const uint32_t a1 = vst + vtaddr + (cst ? 0u : (uint32_t)((32 * pp + C::E_ROWS) * C::ROWB));
-                vt[pp][0] = tr_read<0>(a0);
-                vt[pp][1] = tr_read<0>(a1);
+                vt[pp][0] = tr_read<SI>(vtad[pp][0] + so);
+                vt[pp][1] = tr_read<SI>(vtad[pp][1] + so);
             }
         });
     };
@@ -554,9 +586,12 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     // and, on the matrix cores meanwhile, the scores of tile t+1; the row
     // max of tile t+1 then runs under the PV products.  Scores of tile t
     // live in sc, those of tile t+1 go to sn.  NEXT: there is a tile t+1;
-    // MASK: it may be the ragged last tile.
-    auto iteration = [&](int t, f32x16 (&sc)[NKB], f32x16 (&sn)[NKB], auto next_c, auto mask_c) {
+    // MASK: it may be the ragged last tile.  Tile t sits in stage S when S
+    // >= 0, else in stage t % NST.
+    auto iteration = [&](int t, f32x16 (&sc)[NKB], f32x16 (&sn)[NKB], auto next_c, auto mask_c, auto stage_c) {
         constexpr bool NEXT = decltype(next_c)::value, MASK = decltype(mask_c)::value;
+        constexpr int S = decltype(stage_c)::value;
+        using SNext = std::integral_constant<int, S >= 0 ? (S + 1) % NST : -1>;
         if constexpr (NEXT) {
             // Tile t+1 must have landed (tile t+2 may still be in flight with
             // four stages) before anyone reads it: each wave waits for its own
@@ -569,16 +604,16 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
             asm volatile("" ::: "memory");  // no LDS access moves across the barrier
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            if (t + NST - 1 < ntiles) load_tile(t + NST - 1, (t + NST - 1) % NST);
+            if (t + NST - 1 < ntiles) load_tile(t + NST - 1, S >= 0 ? (S + NST - 1) % NST : (t + NST - 1) % NST);
         }
         // the K operand reads of tile t+1 go first: LDS reads complete in
         // issue order, so V^T reads issued before them would hold the QK
         // products back behind the whole V^T batch
         bf16x8 pb[NKS];
         weights(sc, pb);
-        if constexpr (NEXT) qk(t + 1, sn);
+        if constexpr (NEXT) qk(t + 1, sn, SNext{});
         u32x2 vr[NKS][C::DBLK][2], vt[NPT > 0 ? NPT : 1][2];
-        read_vt(t, vr, vt);
+        read_vt(t, vr, vt, stage_c);
         float mx = 0.f;
         if constexpr (NEXT) {
             if constexpr (MASK) mask(t + 1, sn);
@@ -589,6 +624,11 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
     };
     using T_ = std::true_type;
     using F_ = std::false_type;
+    using RS = std::integral_constant<int, -1>;  // stage known at run time
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using S2 = std::integral_constant<int, 2>;
+    using S3 = std::integral_constant<int, 3>;
 
     // Prologue: the first NST-1 tiles load whether or not this sweep has
     // that many (a tile past the sequence end reads zeros, one past this
@@ -607,7 +647,7 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk) {
             const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
-            qf[kk] = *(const bf16x8*)(stage(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
+            qf[kk] = *(const bf16x8*)(kreg(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
         }
     } else {
         // the compiler waits here for the register loads (all older than
@@ -617,26 +657,34 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" : "+v"(qf[kk]));
     }
     if (ntiles > 0) {
-        qk(0, sA);
+        qk(0, sA, S0{});
         mask(0, sA);
         update_max(row_max(sA));
     }
-    // pairs of iterations whose next tile is not the last one, then the
-    // last one to three tiles
+    // runs of four iterations (stages 0..3) whose next tile is not the
+    // last one, then at most one such pair, then the last one to three
+    // tiles
     int t = 0;
-    for (; t + 3 < ntiles; t += 2) {
-        iteration(t, sA, sB, T_{}, F_{});
-        iteration(t + 1, sB, sA, T_{}, F_{});
+    for (; t + 5 < ntiles; t += 4) {
+        iteration(t, sA, sB, T_{}, F_{}, S0{});
+        iteration(t + 1, sB, sA, T_{}, F_{}, S1{});
+        iteration(t + 2, sA, sB, T_{}, F_{}, S2{});
+        iteration(t + 3, sB, sA, T_{}, F_{}, S3{});
+    }
+    if (t + 3 < ntiles) {
+        iteration(t, sA, sB, T_{}, F_{}, RS{});
+        iteration(t + 1, sB, sA, T_{}, F_{}, RS{});
+        t += 2;
     }
     if (t + 3 == ntiles) {
-        iteration(t, sA, sB, T_{}, F_{});
-        iteration(t + 1, sB, sA, T_{}, T_{});
-        iteration(t + 2, sA, sB, F_{}, F_{});
+        iteration(t, sA, sB, T_{}, F_{}, RS{});
+        iteration(t + 1, sB, sA, T_{}, T_{}, RS{});
+        iteration(t + 2, sA, sB, F_{}, F_{}, RS{});
     } else if (t + 2 == ntiles) {
-        iteration(t, sA, sB, T_{}, T_{});
-        iteration(t + 1, sB, sA, F_{}, F_{});
+        iteration(t, sA, sB, T_{}, T_{}, RS{});
+        iteration(t + 1, sB, sA, F_{}, F_{}, RS{});
     } else if (t + 1 == ntiles) {
-        iteration(t, sA, sB, F_{}, F_{});
+        iteration(t, sA, sB, F_{}, F_{}, RS{});
     }
     // Every wave is done with the stages, and no tile load is in flight
     // (with fewer than NST-1 tiles the prologue's spare loads are still

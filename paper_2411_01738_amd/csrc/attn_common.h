@@ -98,6 +98,12 @@ __device__ __forceinline__ u32x2 tr_read(uint32_t a) {
     asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(a), "i"(OFF));
     return r;
 }
+// An ordinary LDS load at byte address a: the compiler places its wait and
+// folds a constant part of a into the instruction's offset.
+template <typename T>
+__device__ __forceinline__ T lds_ld(uint32_t a) {
+    return *reinterpret_cast<const __attribute__((address_space(3))) T*>(a);
+}
 // A 16-byte LDS read at byte address a + OFF, issued without a wait (the
 // caller waits for it by lgkmcnt).
 template <int OFF>
