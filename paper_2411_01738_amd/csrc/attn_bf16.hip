@@ -150,7 +150,7 @@ struct Cfg {
 
 // One segment: K/V tiles [tile0, tile0 + nt) of the sweep of pair `pair`;
 // pslot: where its partial goes, nullptr for a whole sweep.
-template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS>
+template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS, bool PING>
 __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, int pair, int tile0, int nt,
                                              float* pslot) {
     using C = Cfg<D, QB, KS, KW>;
@@ -656,6 +656,92 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk) asm volatile("" : "+v"(qf[kk]));
     }
+    if constexpr (PING) {
+        // Ping-pong of the two halves of the workgroup (waves w and w + NW/2
+        // share a SIMD): each iteration is a matrix phase (scores of tile
+        // t+1, PV of tile t) and a softmax phase (row max, reference max,
+        // weights of tile t+1), each opened by a workgroup barrier.  The
+        // second half passes one barrier more at the start and the first
+        // half one more at the end, so that between two barriers one half
+        // runs its matrix phase while the other runs its softmax phase, and
+        // the matrix cores and the vector ALUs of a SIMD work at once.
+        // Every wave passes 2 * ntiles + 3 barriers.
+        //   Loads: a wave issues its share of tile t+NST-1 at the start of
+        // its matrix phase t (the stage of tile t-1, whose last reads, the
+        // V^T of tile t-1 in both halves' matrix phase t-1, lie behind the
+        // barrier).  Tile t+1 is first read by the first half's matrix
+        // phase t; every wave has its share of it landed before the barrier
+        // that opens that phase, which is where the first half opens its
+        // matrix phase t and the second half its softmax phase t.
+        const bool lead = wave < C::NW / 2;
+        // nothing moves across the barrier: LDS accesses (memory clobber)
+        // nor arithmetic (scheduling barrier)
+        auto bar = [&]() {
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            asm volatile("" ::: "memory");
+        };
+        // the weights are computed in the softmax phase, not in the next
+        // matrix phase
+        auto pin_pb = [&](bf16x8 (&w)[NKS]) {
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) asm volatile("" : "+v"(w[ks]));
+        };
+        // this wave's loads of tile n have landed; tile n+1's may be in
+        // flight when this segment has it
+        auto landed = [&](int n) {
+            if (n + 1 < ntiles) wait_tiles(std::integral_constant<int, 1>{});
+            else wait_vmem<0>();
+        };
+        bf16x8 pb[NKS];
+        if (!lead) bar();
+        if (ntiles > 0) qk(0, sA, S0{});
+        if (!lead) landed(1);
+        bar();
+        if (ntiles > 0) {
+            mask(0, sA);
+            update_max(row_max(sA));
+            weights(sA, pb);
+            pin_pb(pb);
+        }
+        auto iter_pp = [&](int t, auto next_c, auto mask_c, auto stage_c) {
+            constexpr bool NEXT = decltype(next_c)::value, MASK = decltype(mask_c)::value;
+            constexpr int S = decltype(stage_c)::value;
+            using SNext = std::integral_constant<int, S >= 0 ? (S + 1) % NST : -1>;
+            if (lead) landed(t + 1);
+            bar();
+            if (t + NST - 1 < ntiles) load_tile(t + NST - 1, S >= 0 ? (S + NST - 1) % NST : (t + NST - 1) % NST);
+            if constexpr (NEXT) qk(t + 1, sA, SNext{});
+            u32x2 vr[NKS][C::DBLK][2], vt[NPT > 0 ? NPT : 1][2];
+            read_vt(t, vr, vt, stage_c);
+            pv(vr, vt, pb);
+            if (!lead) landed(t + 2);
+            bar();
+            if constexpr (NEXT) {
+                if constexpr (MASK) mask(t + 1, sA);
+                update_max(row_max(sA));
+                weights(sA, pb);
+                pin_pb(pb);
+            }
+        };
+        int t = 0;
+        for (; t + 5 < ntiles; t += 4) {
+            iter_pp(t, T_{}, F_{}, S0{});
+            iter_pp(t + 1, T_{}, F_{}, S1{});
+            iter_pp(t + 2, T_{}, F_{}, S2{});
+            iter_pp(t + 3, T_{}, F_{}, S3{});
+        }
+        for (; t + 2 < ntiles; ++t) iter_pp(t, T_{}, F_{}, RS{});
+        if (t + 2 == ntiles) {
+            iter_pp(t, T_{}, T_{}, RS{});
+            iter_pp(t + 1, F_{}, F_{}, RS{});
+        } else if (t + 1 == ntiles) {
+            iter_pp(t, F_{}, F_{}, RS{});
+        }
+        if (lead) bar();
+    } else {
     if (ntiles > 0) {
         qk(0, sA, S0{});
         mask(0, sA);
@@ -685,6 +771,7 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         iteration(t + 1, sB, sA, F_{}, F_{}, RS{});
     } else if (t + 1 == ntiles) {
         iteration(t, sA, sB, F_{}, F_{}, RS{});
+    }
     }
     // Every wave is done with the stages, and no tile load is in flight
     // (with fewer than NST-1 tiles the prologue's spare loads are still
@@ -926,12 +1013,12 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 // Workgroups of 4 waves (one per SIMD) are built to run two per CU: each
 // wave is then held to 256 registers, so that every SIMD interleaves two
 // waves of independent workgroups, which no barrier keeps in step.
-template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS>
+template <int D, int QB, int KS, int KW, bool PATCH, bool PARTS, bool PING>
 __global__ __launch_bounds__(64 * QB * KS, QB * KS == 4 ? 2 : 1) void attn_bf16_kernel(Args a) {
     using C = Cfg<D, QB, KS, KW>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[C::LDS_BYTES];
     if constexpr (!PARTS) {
-        attn_segment<D, QB, KS, KW, PATCH, false>(a, lds, xcd_remap(blockIdx.x, gridDim.x), 0, a.T, nullptr);
+        attn_segment<D, QB, KS, KW, PATCH, false, PING>(a, lds, xcd_remap(blockIdx.x, gridDim.x), 0, a.T, nullptr);
         return;
     }
     const int G2 = gridDim.x - a.G1;
@@ -952,7 +1039,7 @@ __global__ __launch_bounds__(64 * QB * KS, QB * KS == 4 ? 2 : 1) void attn_bf16_
         const int nt = (int)min((int64_t)(a.T - t0), ue - u);
         float* slot = t0 == 0 && nt == a.T ? nullptr : a.part + (int64_t)(u == ub ? j : G2 + j) * C::SLOT_FLOATS;
         if (u != ub) __syncthreads();  // the previous segment is done with LDS
-        attn_segment<D, QB, KS, KW, PATCH, true>(a, lds, pair, t0, nt, slot);
+        attn_segment<D, QB, KS, KW, PATCH, true, PING>(a, lds, pair, t0, nt, slot);
         u += nt;
     }
 }
@@ -1143,7 +1230,7 @@ hipError_t launch_fixup(const AttnParams& p, int q_tiles, int T, hipStream_t s) 
     return hipGetLastError();
 }
 
-template <int D, int QB, int KS, int KW, bool PATCH>
+template <int D, int QB, int KS, int KW, bool PATCH, bool PING = false>
 hipError_t launch(const AttnParams& p, hipStream_t s) {
     using C = Cfg<D, QB, KS, KW>;
     Args a;
@@ -1180,7 +1267,7 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
     if (pairs == 0) return hipSuccess;
     const bool parts = p.parts > 0;
     if (!parts) {
-        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, false>), dim3((unsigned)pairs), dim3(C::THREADS),
+        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, false, PING>), dim3((unsigned)pairs), dim3(C::THREADS),
                            0, s, a);
         return hipGetLastError();
     }
@@ -1188,7 +1275,7 @@ hipError_t launch(const AttnParams& p, hipStream_t s) {
         return hipErrorInvalidValue;  // only the 128-row shape runs partitioned launches (slot layout)
     } else {
         if (p.whole < 0 || p.whole > pairs || p.whole % 8 != 0) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, true>), dim3((unsigned)(p.whole + p.parts)),
+        hipLaunchKernelGGL((attn_bf16_kernel<D, QB, KS, KW, PATCH, true, PING>), dim3((unsigned)(p.whole + p.parts)),
                            dim3(C::THREADS), 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -1229,6 +1316,7 @@ static int attn_kernel_choice(int D) {
     if (e != nullptr && strcmp(e, "w64") == 0) return 64;
     if (e != nullptr && strcmp(e, "o2") == 0) return 2;
     if (e != nullptr && strcmp(e, "w32") == 0) return 32;
+    if (e != nullptr && strcmp(e, "pp") == 0) return 3;
     return D > 96 ? 2 : 32;
 }
 
@@ -1240,6 +1328,10 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
         // keep the 8-wave shape (128-row slots)
         if constexpr (D > 96) return launch<D, 4, 1, 32, PATCH>(p, s);
         else if (p.parts <= 0) return launch<D, 2, 2, 32, PATCH>(p, s);
+    }
+    if (attn_kernel_choice(D) == 3) {
+        if constexpr (D > 96) return launch<D, 4, 2, 32, PATCH, true>(p, s);
+        else return launch<D, 4, 2, 64, PATCH, true>(p, s);
     }
     if constexpr (D > 96) {
         return launch<D, 4, 2, 32, PATCH>(p, s);

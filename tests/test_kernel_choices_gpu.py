@@ -1,9 +1,10 @@
 """Parity of each bf16 attention decomposition, forced with
 XDIT_ATTN_KERNEL whatever the default for the head dim: "o2" (workgroups of
-4 waves, two per CU), "w32" (8-wave workgroups) and "w64" (64 query rows per
-wave with the output accumulators in AGPRs, head dim 128), on the chunk
-step, the patch step, the ring step and partitioned launches, against the
-fp64 oracle.  The library's default choice runs every other GPU test."""
+4 waves, two per CU), "w32" (8-wave workgroups), "pp" (8-wave workgroups
+whose two halves alternate matrix and softmax phases) and "w64" (64 query
+rows per wave with the output accumulators in AGPRs, head dim 128), on the
+chunk step, the patch step, the ring step and partitioned launches, against
+the fp64 oracle.  The library's default choice runs every other GPU test."""
 from __future__ import annotations
 
 import numpy as np
@@ -17,7 +18,7 @@ from tests.gpu_util import check_lse, check_out, to_gpu, to_np, torch_mod
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(params=["o2", "w32", "w64"])
+@pytest.fixture(params=["o2", "w32", "pp", "w64"])
 def choice(request, monkeypatch):
     monkeypatch.setenv("XDIT_ATTN_KERNEL", request.param)
     return request.param
