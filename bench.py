@@ -18,12 +18,13 @@ Prints ONE JSON line.
 `value` is algorithmic attention FLOP/s (4*B*H*Nq*Nk*d per call) over the
 whole step.  `roofline` refers to the kernel with the largest share of the
 step's time: `achieved` and `frac` are timed with HIP events live in this
-run; `traffic` (HBM bytes) and `mfma_busy` come from rocprofv3 counter runs
-of the same kernel build, named in `traffic_source`, and are null for any
-other build.  `cpu_baseline` times the fp64 oracle on a bounded row sample of
-the same workload on the host's cores.  With the default pixart workload the
-line also carries `flux_16k`: the same measurement of the Flux 2048px
-sequence-parallel share (16896 tokens), the 16k-token configuration.
+run; `traffic` (HBM bytes per launch) and `mfma_busy` come from rocprofv3
+counter runs of the same kernel build, whose summaries `traffic_source` and
+`counters_source` name, and are null for any other build.  `cpu_baseline`
+times the fp64 oracle on a bounded row sample of the same workload on the
+host's cores.  With the default pixart workload the line also carries
+`flux_16k`: the same measurement of the Flux 2048px sequence-parallel share
+(16896 tokens), the 16k-token configuration.
 """
 from __future__ import annotations
 
@@ -47,23 +48,32 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # kernel build it was taken on (sha256 prefix of the source and its compile
 # flags); a different build reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (49151 + 13875) * 1024, "src": "0ae64fdbe1062094"},
-    ("sd3", "patch_attn"): {"bytes": (58953 + 9216) * 1024, "src": "0ae64fdbe1062094"},
+    ("pixart", "patch_attn"): {"bytes": (49381 + 13872) * 1024, "src": "6466465c6fff344e"},
+    ("sd3", "patch_attn"): {"bytes": (59079 + 9216) * 1024, "src": "6466465c6fff344e"},
     # the partitioned sweep and its fix-up, one launch of each per call
-    ("flux", "chunk_attn"): {"bytes": (154455 + 41224) * 1024, "src": "0ae64fdbe1062094"},
-    ("flux_ring", "chunk_attn"): {"bytes": (135360 + 25763) * 1024, "src": "0ae64fdbe1062094"},
-    ("cog", "patch_attn"): {"bytes": (264983 + 19744) * 1024, "src": "0ae64fdbe1062094"},
-    ("cog", "chunk_attn"): {"bytes": (133307 + 109989) * 1024, "src": "0ae64fdbe1062094"},
+    ("flux", "chunk_attn"): {"bytes": (139967 + 41225) * 1024, "src": "6466465c6fff344e"},
+    ("flux_ring", "chunk_attn"): {"bytes": (158662 + 41277) * 1024, "src": "6466465c6fff344e"},
+    ("cog", "patch_attn"): {"bytes": (265105 + 19745) * 1024, "src": "6466465c6fff344e"},
+    ("cog", "chunk_attn"): {"bytes": (133364 + 109989) * 1024, "src": "6466465c6fff344e"},
 }
 
 
-def traffic_of(workload: str, kind: str):
+TRAFFIC_FILES = {
+    "pixart": "profiles/attn_patch_pixart_hbm_traffic.txt",
+    "sd3": "profiles/attn_patch_sd3_hbm_traffic.txt",
+    "flux": "profiles/attn_chunk_flux_hbm_traffic.txt",
+    "flux_ring": "profiles/attn_chunk_flux_ring_hbm_traffic.txt",
+    "cog": "profiles/attn_patch_cog_hbm_traffic.txt",
+}
+
+
+def traffic_of(workload: str, kind: str) -> dict:
     from paper_2411_01738_amd.build import kernel_fingerprint
 
     e = MEASURED_TRAFFIC.get((workload, kind))
-    if e is None:
-        return None
-    return e["bytes"] if kernel_fingerprint() == e["src"] else None
+    if e is None or kernel_fingerprint() != e["src"]:
+        return {"traffic": None, "traffic_source": None}
+    return {"traffic": e["bytes"], "traffic_source": TRAFFIC_FILES[workload]}
 
 
 # Matrix-core counters of the dominant kernel from a rocprofv3 --pmc run of
@@ -71,7 +81,18 @@ def traffic_of(workload: str, kind: str):
 # the fraction of the kernel's CU-busy time the matrix pipes worked), with the
 # summary file and the kernel build's fingerprint; a different build reports
 # nothing.
-MEASURED_COUNTERS = {}
+MEASURED_COUNTERS = {
+    ("pixart", "patch_attn"): {"mfma_busy": 0.380, "file": "profiles/attn_patch_pixart_mfma_counters.txt",
+                               "src": "6466465c6fff344e"},
+    ("sd3", "patch_attn"): {"mfma_busy": 0.356, "file": "profiles/attn_patch_sd3_mfma_counters.txt",
+                            "src": "6466465c6fff344e"},
+    ("flux", "chunk_attn"): {"mfma_busy": 0.532, "file": "profiles/attn_chunk_flux_mfma_counters.txt",
+                             "src": "6466465c6fff344e"},
+    ("cog", "patch_attn"): {"mfma_busy": 0.408, "file": "profiles/attn_patch_cog_mfma_counters.txt",
+                            "src": "6466465c6fff344e"},
+    ("cog", "chunk_attn"): {"mfma_busy": 0.358, "file": "profiles/attn_patch_cog_mfma_counters.txt",
+                            "src": "6466465c6fff344e"},
+}
 
 
 def counters_of(workload: str, kind: str) -> dict:
@@ -79,8 +100,8 @@ def counters_of(workload: str, kind: str) -> dict:
 
     e = MEASURED_COUNTERS.get((workload, kind))
     if e is None or kernel_fingerprint() != e["src"]:
-        return {"traffic_source": None, "mfma_busy": None}
-    return {"traffic_source": e["file"], "mfma_busy": e["mfma_busy"]}
+        return {"mfma_busy": None, "counters_source": None}
+    return {"mfma_busy": e["mfma_busy"], "counters_source": e["file"]}
 
 
 def parse():
@@ -407,7 +428,7 @@ def measure(w, t, steps: int, warmup: int, split: bool, extra_timings: bool = Tr
         achieved = per_launch / avg_s / 1e9
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = traffic_of(w.name, dom)
+    roof.update(traffic_of(w.name, dom))
     roof["timing"] = timing
     roof.update(counters_of(w.name, dom))
     hp = None
