@@ -9,8 +9,10 @@ workload (default: Pixart 1024px, B=2 H=16 d=72, 4096 tokens):
   * the sequence-parallel share: chunk attention of the local query shard over
     each K/V chunk (O and LSE), then the LSE merge of the partials.
 Inputs are synthetic (seeded N(0,1); stale K/V = fresh + N(0, 0.05^2)) and
-resident in HBM before timing starts.  W untimed steps (the default lets the
-GPU clocks settle), then K timed steps between synchronisations with events
+resident in HBM before timing starts.  A clock pre-heat (whole steps for
+--preheat-s seconds of wall time, 0.3 by default: a GPU that was idle runs
+its first tens of milliseconds of work at lower clocks), then W untimed
+steps, then K timed steps between synchronisations with events
 only at the ends; then K more steps with HIP events around each run of
 consecutive launches of one kernel give each kernel's average duration.
 Prints ONE JSON line.
@@ -109,6 +111,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--preheat-s", type=float, default=0.3,
+                    help="seconds of untimed whole steps before the warm-up steps (clock ramp)")
     ap.add_argument("--workload", default="pixart",
                     choices=["tiny", "pixart", "sd3", "flux", "cog", "sd3_ic", "sd3_ic_bal", "pixart_hybrid",
                              "pixart_stage",
@@ -239,8 +243,9 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def measure(w, t, steps: int, warmup: int, split: bool, extra_timings: bool = True):
-    """Time one workload on the GPU: `warmup` untimed steps, then exactly
+def measure(w, t, steps: int, warmup: int, split: bool, extra_timings: bool = True, preheat_s: float = 0.0):
+    """Time one workload on the GPU: whole steps for `preheat_s` seconds and
+    `warmup` more, all untimed, then exactly
     `steps` timed steps between synchronisations (events only at the two
     ends), then `steps` more with HIP events around each run of consecutive
     launches of one kernel.  Returns the step figures, per-kernel figures and
@@ -264,6 +269,13 @@ def measure(w, t, steps: int, warmup: int, split: bool, extra_timings: bool = Tr
         if not w.sp_ring:
             calls.append(("lse_merge", hp.merge, 0.0, hp.merge_bytes()))
 
+    # clock pre-heat: the GPU leaves its idle clocks during the first tens of
+    # milliseconds of sustained work; untimed, before the warm-up steps
+    t_end = time.perf_counter() + preheat_s
+    while time.perf_counter() < t_end:
+        for _ in range(10):
+            hp.step()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         hp.step()
     torch.cuda.synchronize()
@@ -479,7 +491,7 @@ def main():
     torch.cuda.set_device(0)
     w = WORKLOADS[args.workload]
     t = generate(w)
-    m = measure(w, t, args.steps, args.warmup, not args.no_split)
+    m = measure(w, t, args.steps, args.warmup, not args.no_split, preheat_s=args.preheat_s)
 
     # the 16k-token target configuration (Flux SP share) beside the headline
     # one, under the same clock: same K and W, its own per-kernel figures,
@@ -488,7 +500,8 @@ def main():
     if args.workload == "pixart" and not args.no_flux:
         wf = WORKLOADS["flux"]
         tf = generate(wf)
-        mf = measure(wf, tf, args.steps, args.warmup, not args.no_split, extra_timings=True)
+        mf = measure(wf, tf, args.steps, args.warmup, not args.no_split, extra_timings=True,
+                     preheat_s=args.preheat_s)
         flux = {"workload": DESC["flux"], "value": round(mf["value"], 2), "unit": "TFLOP/s",
                 "ms_per_step": round(mf["ms_per_step"], 4), "flops_per_step": mf["step_flops"],
                 "kernels": mf["kernels"], "roofline": mf["roofline"]}
@@ -507,6 +520,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "preheat_s": args.preheat_s,
         "ms_per_step": round(m["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
