@@ -1295,20 +1295,24 @@ double fill(int64_t blocks) {
     return rounds ? (double)blocks / (double)(rounds * kCUs) : 1.0;
 }
 
-// XDIT_ATTN_TILE forces one shape (tuning and tests): "wide" or "narrow"
-// (narrow falls back to wide at d = 128); anything else, or unset, picks by
-// the fill estimate.
+// XDIT_ATTN_TILE forces one shape (tuning and tests): "wide", "narrow"
+// (8 waves; both fall back to the default at d = 128) or "quad" (4 waves,
+// 128 rows, 64-key tiles; d = 64 only, unpartitioned launches); anything
+// else, or unset, picks by the fill estimate.
 int forced_shape() {
     const char* e = getenv("XDIT_ATTN_TILE");
     if (e == nullptr) return 0;
     if (strcmp(e, "wide") == 0) return 1;
     if (strcmp(e, "narrow") == 0) return 2;
+    if (strcmp(e, "quad") == 0) return 3;
     return 0;
 }
 
 // XDIT_ATTN_KERNEL selects the decomposition: "w64" (64 query rows per
 // wave, attn_w64.hip, head dim 128), "o2" (workgroups of 4 waves, two per
-// CU) or "w32" (the 8-wave workgroups of this file).  Unset: o2 at d = 128
+// CU), "w32" (the 8-wave workgroups of this file, and at d = 64 the 4-wave
+// 128-row shape where the grid has more query tiles than CUs) or "pp" (the
+// 8-wave shapes with the two halves in ping-pong).  Unset: o2 at d = 128
 // (the Flux chunk step measured 221 vs 228-236 us), w32 at d <= 72 (o2's
 // 64-row, 64-key shape measured 10-18 % slower there).
 static int attn_kernel_choice(int D) {
@@ -1337,11 +1341,23 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
         return launch<D, 4, 2, 32, PATCH>(p, s);
     } else {
         const int forced = forced_shape();
+        const int64_t bh = (int64_t)p.B * p.H;
+        const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
+        if constexpr (D == 64) {
+            // More 128-row query tiles than CUs: workgroups of 4 waves (128
+            // rows, one key split, 64-key tiles), two per CU, whose waves
+            // interleave on each SIMD as at d = 128 (cog chunk step 630 ->
+            // 543 us, patch step 317 -> 308 us).  With no more tiles than
+            // CUs most CUs would get one such workgroup, one wave per SIMD
+            // (sd3 patch step 44 -> 52 us), and the 8-wave shapes stay.
+            // (d = 72 needs the query tile in LDS, which a 64-key region
+            // cannot hold.)
+            if (p.parts <= 0 && (forced == 3 || (forced == 0 && wide > kCUs)))
+                return launch<D, 4, 1, 64, PATCH>(p, s);
+        }
         // split keys fill the GPU by themselves: 128-row query tiles
         if (forced == 1 || p.parts > 0) return launch<D, 4, 2, 64, PATCH>(p, s);
         if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);
-        const int64_t bh = (int64_t)p.B * p.H;
-        const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
         const double qfill_w = (double)p.Nq / ((p.Nq + 127) / 128 * 128.0);
         const double qfill_n = (double)p.Nq / ((p.Nq + 63) / 64 * 64.0);
         if (fill(narrow) * qfill_n > 1.1 * fill(wide) * qfill_w) return launch<D, 2, 4, 32, PATCH>(p, s);

@@ -24,11 +24,12 @@ def torch():
     return torch_mod()
 
 
-@pytest.fixture(params=["auto", "wide", "narrow"])
+@pytest.fixture(params=["auto", "wide", "narrow", "quad"])
 def tile_shape(request, monkeypatch):
-    """Workgroup shape of the bf16 kernel: 128 query rows x 2 key splits
-    ("wide"), 64 x 4 ("narrow", head dim <= 72; d = 128 always runs wide), or
-    the library's own choice."""
+    """Workgroup shape of the bf16 kernel at head dim <= 72: 128 query rows x
+    2 key splits ("wide"), 64 x 4 ("narrow"), 4 waves of 128 rows over 64-key
+    tiles ("quad", d = 64 only; others fall back to the library's choice), or
+    the library's own choice.  d = 128 runs its own shape in all four."""
     if request.param == "auto":
         monkeypatch.delenv("XDIT_ATTN_TILE", raising=False)
     else:
@@ -56,8 +57,9 @@ CHUNK_CASES = [
     ("bf16", 1, 1, 1, 1, 64),
     ("bf16", 1, 5, 64, 1, 72),
     ("bf16", 1, 128, 128, 1, 128),
-    # K/V tile counts 3..11, whole and ragged (tiles of 128 keys at d <= 72,
-    # 64 at d = 128), so that every way the tile loop can end is taken
+    # K/V tile counts 3..22, whole and ragged (tiles of 128 keys in the
+    # 8-wave shapes at d <= 72, 64 in the 4-wave one at d = 64, 32 at
+    # d = 128), so that every way the tile loop can end is taken
     ("bf16", 1, 40, 384, 1, 64),
     ("bf16", 1, 100, 512, 2, 64),
     ("bf16", 1, 70, 645, 2, 72),
