@@ -15,7 +15,10 @@
 //     BN = KS*KW-key tile).  The KS waves of a query block keep separate
 //     running (max, sum, output) and are merged through LDS at the end, like
 //     the chunk partials of the sequence-parallel merge.  Two waves per SIMD
-//     let one wave's matrix work overlap another's softmax;
+//     let one wave's matrix work overlap another's softmax.  Shapes: 8
+//     waves of 128 rows x 2 splits or 64 rows x 4 splits over 128-key tiles
+//     (d <= 72, one workgroup per CU); 4 waves of 128 rows over 64-key (d =
+//     64) or 32-key (d = 128) tiles, two workgroups per CU;
 //   * K/V tiles go from memory straight into LDS (buffer loads with an LDS
 //     destination: no registers, no LDS store instructions), NSTAGE tiles
 //     deep, so the loads of the next tiles are in flight while tile t is
@@ -40,10 +43,11 @@
 //     read from the row-major V tile with ds_read_b64_tr_b16, which hands
 //     each lane one head dimension of four keys, the keys chosen to match
 //     P's register order;
-//   * where the output rows are padded (d = 72 -> 96), the padding lanes read
-//     a constant chunk in LDS: dimension 72 reads ones, so the same MFMA
-//     also produces the row sums of the bf16 weights (the exact normaliser
-//     of the bf16 numerator), the rest read zeros.
+//   * at d = 72 dims 64..71 run as one 16-row tail block on
+//     v_mfma_f32_16x16x32_bf16, whose padding lanes read a constant chunk in
+//     LDS: dimension 72 reads ones, so the same product also yields the row
+//     sums of the bf16 weights (the exact normaliser of the bf16
+//     numerator), the rest read zeros.
 // Workgroups are renumbered so that all query tiles of one (batch, head) run
 // on the same XCD and share its L2 for K/V (the hardware deals workgroup ids
 // round-robin over the 8 XCDs).
@@ -742,36 +746,36 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
         }
         if (lead) bar();
     } else {
-    if (ntiles > 0) {
-        qk(0, sA, S0{});
-        mask(0, sA);
-        update_max(row_max(sA));
-    }
-    // runs of four iterations (stages 0..3) whose next tile is not the
-    // last one, then at most one such pair, then the last one to three
-    // tiles
-    int t = 0;
-    for (; t + 5 < ntiles; t += 4) {
-        iteration(t, sA, sB, T_{}, F_{}, S0{});
-        iteration(t + 1, sB, sA, T_{}, F_{}, S1{});
-        iteration(t + 2, sA, sB, T_{}, F_{}, S2{});
-        iteration(t + 3, sB, sA, T_{}, F_{}, S3{});
-    }
-    if (t + 3 < ntiles) {
-        iteration(t, sA, sB, T_{}, F_{}, RS{});
-        iteration(t + 1, sB, sA, T_{}, F_{}, RS{});
-        t += 2;
-    }
-    if (t + 3 == ntiles) {
-        iteration(t, sA, sB, T_{}, F_{}, RS{});
-        iteration(t + 1, sB, sA, T_{}, T_{}, RS{});
-        iteration(t + 2, sA, sB, F_{}, F_{}, RS{});
-    } else if (t + 2 == ntiles) {
-        iteration(t, sA, sB, T_{}, T_{}, RS{});
-        iteration(t + 1, sB, sA, F_{}, F_{}, RS{});
-    } else if (t + 1 == ntiles) {
-        iteration(t, sA, sB, F_{}, F_{}, RS{});
-    }
+        if (ntiles > 0) {
+            qk(0, sA, S0{});
+            mask(0, sA);
+            update_max(row_max(sA));
+        }
+        // runs of four iterations (stages 0..3) whose next tile is not the
+        // last one, then at most one such pair, then the last one to three
+        // tiles
+        int t = 0;
+        for (; t + 5 < ntiles; t += 4) {
+            iteration(t, sA, sB, T_{}, F_{}, S0{});
+            iteration(t + 1, sB, sA, T_{}, F_{}, S1{});
+            iteration(t + 2, sA, sB, T_{}, F_{}, S2{});
+            iteration(t + 3, sB, sA, T_{}, F_{}, S3{});
+        }
+        if (t + 3 < ntiles) {
+            iteration(t, sA, sB, T_{}, F_{}, RS{});
+            iteration(t + 1, sB, sA, T_{}, F_{}, RS{});
+            t += 2;
+        }
+        if (t + 3 == ntiles) {
+            iteration(t, sA, sB, T_{}, F_{}, RS{});
+            iteration(t + 1, sB, sA, T_{}, T_{}, RS{});
+            iteration(t + 2, sA, sB, F_{}, F_{}, RS{});
+        } else if (t + 2 == ntiles) {
+            iteration(t, sA, sB, T_{}, T_{}, RS{});
+            iteration(t + 1, sB, sA, F_{}, F_{}, RS{});
+        } else if (t + 1 == ntiles) {
+            iteration(t, sA, sB, F_{}, F_{}, RS{});
+        }
     }
     // Every wave is done with the stages, and no tile load is in flight
     // (with fewer than NST-1 tiles the prologue's spare loads are still
