@@ -7,9 +7,11 @@
  * ---------------------------------------
  * Pointers: every tensor pointer is a DEVICE pointer, owned by the caller, at
  *   least 16-byte aligned, to dense row-major storage.  The library allocates
- *   nothing and keeps no state except a per-thread stream and error message.
- *   The one exception is xdit_lse_merge's `outs` / `lses`, which are HOST
- *   arrays holding `n` device pointers.
+ *   nothing and keeps no state except a per-thread stream and error message,
+ *   the GEMM plans of xdit_stage_step (hipBLASLt's own memory) and the static
+ *   scratch array of xdit_chunk_attn_split_noalloc.  The one exception is
+ *   xdit_lse_merge's `outs` / `lses`, which are HOST arrays holding `n`
+ *   device pointers.
  * Layouts (the paper fixes none; this is the layout a QKV projection emits):
  *   activations  [B, N, H, d]  sequence-major, d contiguous (q, k, v, out,
  *                              fresh_k, fresh_v, merge partials)
@@ -30,6 +32,12 @@
  *   effects (the K/V buffer is untouched); xdit_last_error() then describes
  *   the problem.  NaN / Inf inputs are not checked and propagate.
  * A pointer may be NULL only where the tensor it stands for has no elements.
+ * Tuning (environment, read at every call; results stay within the same
+ *   tolerance, only the work decomposition changes): XDIT_ATTN_KERNEL = o2 |
+ *   w32 | pp | w64 selects the bf16 attention decomposition, XDIT_ATTN_TILE =
+ *   wide | narrow | quad its workgroup shape at head_dim <= 72, and
+ *   XDIT_PARTITION = none | balanced the partition of *_split calls made with
+ *   splits <= 0.  Unset, the library chooses.
  */
 #ifndef XDIT_H
 #define XDIT_H
