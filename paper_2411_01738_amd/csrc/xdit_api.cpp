@@ -161,7 +161,11 @@ static int64_t part_ws_bytes(const Partition& pt, int64_t pairs, int64_t head_di
 //     cut into s = min(16, 256 / r) parts, so that the last round is full
 //     (K/V reuse among the query tiles of one head is kept in the rounds of
 //     whole sweeps).
-// A partition is taken only when the model saves at least 10 %.
+// A partition is taken only when the model saves at least 10 %.  The model
+// counts rounds of one workgroup per CU; at d = 128 the kernel runs two
+// 4-wave workgroups per CU, for which flux's measured alternatives (whole
+// rounds of 512 with the rest cut, 512 equal ranges) were no faster than
+// this choice.
 // XDIT_PARTITION=balanced instead cuts the whole launch into 256 equal
 // ranges (ranges cross query tiles; it loses the K/V reuse, so it is never
 // chosen; tests use it), XDIT_PARTITION=none forces no partition.
