@@ -88,7 +88,7 @@ def test_chunk_attn(orc, torch, tile_shape, dtype, B, Nq, Nk, H, d):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("d", [64, 72, 128])
-def test_chunk_empty_kv(torch, dtype, d):
+def test_chunk_empty_kv(torch, tile_shape, dtype, d):
     B, Nq, H = 1, 70, 2
     q = to_gpu(random_io((B, Nq, H, d), dtype, 5), dtype)
     e = torch.zeros((B, 0, H, d), device="cuda", dtype=tdtype(dtype))
