@@ -43,6 +43,38 @@ def test_library_exports_every_declared_symbol():
     assert set(_lib.SIGNATURES) == set(header_functions())
 
 
+def test_header_is_plain_c_and_links(tmp_path):
+    """A C99 program that includes the header, takes the address of every
+    declared entry point and links against the library builds cleanly with
+    -Wall -Werror, and runs (it calls only xdit_version, which touches no
+    device)."""
+    import shutil
+    import subprocess
+
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc is not available")
+    lib = _lib.lib()  # built (or fails with the build hint)
+    names = header_functions()
+    src = tmp_path / "abi.c"
+    src.write_text(
+        "#include <stdio.h>\n#include \"xdit.h\"\n"
+        "int main(void) {\n"
+        "    void (*fns[])(void) = {" + ", ".join(f"(void (*)(void))&{n}" for n in names) + "};\n"
+        "    for (unsigned i = 0; i < sizeof fns / sizeof fns[0]; ++i) if (!fns[i]) return 1;\n"
+        "    printf(\"%s\\n\", xdit_version());\n"
+        "    return 0;\n}\n")
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(_lib.LIBRARY)
+    r = subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                        "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                        "-L", libdir, "-lxdit", f"-Wl,-rpath,{libdir}"], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == lib.xdit_version().decode()
+
+
 def test_version_and_stream_roundtrip():
     lib = _lib.lib()
     assert b"gfx950" in lib.xdit_version()
