@@ -126,10 +126,11 @@ struct Cfg {
     static constexpr int DMA_MIN_PER_WAVE = 2 * (DMA_PER_TILE / NW);  // K and V, fewest by any wave
     static constexpr int Q_PIECES = BM * ROWB / 1024;  // 64-lane loads of the query tile
     static constexpr int Q_PER_WAVE = (Q_PIECES + NW - 1) / NW;
-    // the query tile is staged through LDS where it fits a stage's tiles;
-    // otherwise (128 rows of d = 128 over 32-key tiles) each wave loads its
-    // rows straight into registers
-    static constexpr bool Q_LDS = BM * ROWB <= TILE_BYTES;  // in the K region of stage NSTAGE-1
+    // the query tile is staged through LDS where it fits the K and V tiles
+    // of stage NSTAGE-1 (rows 0..BN-1 in its K region, the rest in its V
+    // region); otherwise (128 rows of d = 128 over 32-key tiles) each wave
+    // loads its rows straight into registers
+    static constexpr bool Q_LDS = BM * ROWB <= 2 * TILE_BYTES;
     static constexpr int NKB = KW / 32;              // 32-key blocks of S^T per wave
     static constexpr int NKS = KW / 16;              // 16-key PV steps per wave
     static constexpr bool SUM_BY_MFMA = TAIL;        // a padding row of V^T holds ones
@@ -144,7 +145,7 @@ struct Cfg {
     static_assert(DK - D == 0 || DK - D == 8, "K padding is at most one 16-byte chunk");
     static_assert(!TAIL || (D - TB <= 15 && D - TB > 0 && KW % 32 == 0), "tail block: dims TB..D-1, then the ones row");
     static_assert(KW % 32 == 0, "a wave takes whole 32-key blocks");
-    static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads");
+    static_assert(TILE_BYTES % 1024 == 0, "tiles are whole 64-lane loads (a query load lies in one region)");
     static_assert(DMA_PER_TILE >= NW, "every wave loads part of each tile");
     static_assert(BM * ROWB % 1024 == 0, "the query tile is whole 64-lane loads");
     static_assert(Q_LDS || DK == D, "query rows loaded into registers have no padding chunk");
@@ -210,11 +211,16 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
             (tid & 1) ? u32x4{0x3f80u, 0, 0, 0} : u32x4{0, 0, 0, 0};
     }
 
-    // The query tile goes to LDS stage NST-1, which no K/V tile uses
-    // before iteration 0, in the same load stream as the tiles (issued
-    // first, so the wait for tile 0 covers it); rows past Nq read as zero.
+    // The query tile goes to LDS stage NST-1 (its K region, then its V
+    // region: byte o of the tile at qlds(o), a row boundary between them),
+    // which no K/V tile uses before iteration 0, in the same load stream as
+    // the tiles (issued first, so the wait for tile 0 covers it); rows past
+    // Nq read as zero.
     // Routing it through LDS leaves no register with a vector-memory load
     // outstanding, so the compiler never has to wait on one in the loop.
+    auto qlds = [&](int o) -> unsigned char* {
+        return o < C::TILE_BYTES ? kreg(NST - 1) + o : vreg(NST - 1) + (o - C::TILE_BYTES);
+    };
     const int qrow = qt * C::BM + qb * 32 + c;
     const bool qvalid = qrow < a.Nq;
     const Rsrc ro = rsrc(out_base + (int64_t)b * a.Nq * a.H * D, (uint32_t)a.Nq * rowb);
@@ -230,7 +236,7 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
                 if (C::Q_PIECES % C::NW == 0 || ins < C::Q_PIECES) {
                     // slot p: row p / CH, logical chunk (p % CH) ^ swz(row)
                     const int p = 64 * ins + lane, r = p / C::CH;
-                    dma16(rq, kreg(NST - 1) + 1024 * ins, (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
+                    dma16(rq, qlds(1024 * ins), (uint32_t)r * rowb + 16 * ((p % C::CH) ^ C::swz(r)));
                 }
             }
         } else {
@@ -651,7 +657,7 @@ __device__ __forceinline__ void attn_segment(const Args& a, unsigned char* lds, 
 #pragma unroll
         for (int kk = 0; kk < C::KSTEPS; ++kk) {
             const int r = qb * 32 + c, lc = 2 * kk + hf;  // chunks past d read the zero chunk
-            qf[kk] = *(const bf16x8*)(kreg(NST - 1) + (lc < C::CH ? 16 * (r * C::CH + (lc ^ C::swz(r))) : C::CONST_OFF));
+            qf[kk] = *(const bf16x8*)(lc < C::CH ? qlds(16 * (r * C::CH + (lc ^ C::swz(r)))) : kreg(NST - 1) + C::CONST_OFF);
         }
     } else {
         // the compiler waits here for the register loads (all older than
@@ -1301,8 +1307,8 @@ double fill(int64_t blocks) {
 
 // XDIT_ATTN_TILE forces one shape (tuning and tests): "wide", "narrow"
 // (8 waves; both fall back to the default at d = 128) or "quad" (4 waves,
-// 128 rows, 64-key tiles; d = 64 only, unpartitioned launches); anything
-// else, or unset, picks by the fill estimate.
+// 128 rows, 64-key tiles; d <= 72, unpartitioned launches); anything else,
+// or unset, picks by the fill estimate.
 int forced_shape() {
     const char* e = getenv("XDIT_ATTN_TILE");
     if (e == nullptr) return 0;
@@ -1314,7 +1320,7 @@ int forced_shape() {
 
 // XDIT_ATTN_KERNEL selects the decomposition: "w64" (64 query rows per
 // wave, attn_w64.hip, head dim 128), "o2" (workgroups of 4 waves, two per
-// CU), "w32" (the 8-wave workgroups of this file, and at d = 64 the 4-wave
+// CU), "w32" (the 8-wave workgroups of this file, and at d <= 72 the 4-wave
 // 128-row shape where the grid has more query tiles than CUs) or "pp" (the
 // 8-wave shapes with the two halves in ping-pong).  Unset: o2 at d = 128
 // (the Flux chunk step measured 221 vs 228-236 us), w32 at d <= 72 (o2's
@@ -1347,18 +1353,13 @@ hipError_t dispatch(const AttnParams& p, hipStream_t s) {
         const int forced = forced_shape();
         const int64_t bh = (int64_t)p.B * p.H;
         const int64_t wide = (p.Nq + 127) / 128 * bh, narrow = (p.Nq + 63) / 64 * bh;
-        if constexpr (D == 64) {
-            // More 128-row query tiles than CUs: workgroups of 4 waves (128
-            // rows, one key split, 64-key tiles), two per CU, whose waves
-            // interleave on each SIMD as at d = 128 (cog chunk step 630 ->
-            // 543 us, patch step 317 -> 308 us).  With no more tiles than
-            // CUs most CUs would get one such workgroup, one wave per SIMD
-            // (sd3 patch step 44 -> 52 us), and the 8-wave shapes stay.
-            // (d = 72 needs the query tile in LDS, which a 64-key region
-            // cannot hold.)
-            if (p.parts <= 0 && (forced == 3 || (forced == 0 && wide > kCUs)))
-                return launch<D, 4, 1, 64, PATCH>(p, s);
-        }
+        // More 128-row query tiles than CUs: workgroups of 4 waves (128
+        // rows, one key split, 64-key tiles), two per CU, whose waves
+        // interleave on each SIMD as at d = 128 (cog chunk step 630 -> 543
+        // us, patch step 317 -> 308 us).  With no more tiles than CUs most
+        // CUs would get one such workgroup, one wave per SIMD (sd3 patch
+        // step 44 -> 52 us), and the 8-wave shapes stay.
+        if (p.parts <= 0 && (forced == 3 || (forced == 0 && wide > kCUs))) return launch<D, 4, 1, 64, PATCH>(p, s);
         // split keys fill the GPU by themselves: 128-row query tiles
         if (forced == 1 || p.parts > 0) return launch<D, 4, 2, 64, PATCH>(p, s);
         if (forced == 2) return launch<D, 2, 4, 32, PATCH>(p, s);

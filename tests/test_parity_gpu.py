@@ -28,8 +28,8 @@ def torch():
 def tile_shape(request, monkeypatch):
     """Workgroup shape of the bf16 kernel at head dim <= 72: 128 query rows x
     2 key splits ("wide"), 64 x 4 ("narrow"), 4 waves of 128 rows over 64-key
-    tiles ("quad", d = 64 only; others fall back to the library's choice), or
-    the library's own choice.  d = 128 runs its own shape in all four."""
+    tiles ("quad"), or the library's own choice.  d = 128 runs its own shape
+    in all four."""
     if request.param == "auto":
         monkeypatch.delenv("XDIT_ATTN_TILE", raising=False)
     else:
