@@ -17,8 +17,8 @@
 //     the chunk partials of the sequence-parallel merge.  Two waves per SIMD
 //     let one wave's matrix work overlap another's softmax.  Shapes: 8
 //     waves of 128 rows x 2 splits or 64 rows x 4 splits over 128-key tiles
-//     (d <= 72, one workgroup per CU); 4 waves of 128 rows over 64-key (d =
-//     64) or 32-key (d = 128) tiles, two workgroups per CU;
+//     (d <= 72, one workgroup per CU); 4 waves of 128 rows over 64-key (d
+//     <= 72) or 32-key (d = 128) tiles, two workgroups per CU;
 //   * K/V tiles go from memory straight into LDS (buffer loads with an LDS
 //     destination: no registers, no LDS store instructions), NSTAGE tiles
 //     deep, so the loads of the next tiles are in flight while tile t is
