@@ -50,13 +50,13 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 # kernel build it was taken on (sha256 prefix of the source and its compile
 # flags); a different build reports null.
 MEASURED_TRAFFIC = {
-    ("pixart", "patch_attn"): {"bytes": (49220 + 13877) * 1024, "src": "92e87f5640eb8a6c"},
-    ("sd3", "patch_attn"): {"bytes": (59117 + 9216) * 1024, "src": "92e87f5640eb8a6c"},
+    ("pixart", "patch_attn"): {"bytes": (49251 + 13875) * 1024, "src": "8ea515cefb0f3f25"},
+    ("sd3", "patch_attn"): {"bytes": (59123 + 9216) * 1024, "src": "8ea515cefb0f3f25"},
     # the partitioned sweep and its fix-up, one launch of each per call
-    ("flux", "chunk_attn"): {"bytes": (139855 + 41226) * 1024, "src": "92e87f5640eb8a6c"},
-    ("flux_ring", "chunk_attn"): {"bytes": (158613 + 41264) * 1024, "src": "92e87f5640eb8a6c"},
-    ("cog", "patch_attn"): {"bytes": (259469 + 19744) * 1024, "src": "92e87f5640eb8a6c"},
-    ("cog", "chunk_attn"): {"bytes": (133506 + 109990) * 1024, "src": "92e87f5640eb8a6c"},
+    ("flux", "chunk_attn"): {"bytes": (139907 + 41225) * 1024, "src": "8ea515cefb0f3f25"},
+    ("flux_ring", "chunk_attn"): {"bytes": (158643 + 41277) * 1024, "src": "8ea515cefb0f3f25"},
+    ("cog", "patch_attn"): {"bytes": (259311 + 19744) * 1024, "src": "8ea515cefb0f3f25"},
+    ("cog", "chunk_attn"): {"bytes": (133526 + 109990) * 1024, "src": "8ea515cefb0f3f25"},
 }
 
 
@@ -84,16 +84,16 @@ def traffic_of(workload: str, kind: str) -> dict:
 # summary file and the kernel build's fingerprint; a different build reports
 # nothing.
 MEASURED_COUNTERS = {
-    ("pixart", "patch_attn"): {"mfma_busy": 0.377, "file": "profiles/attn_patch_pixart_mfma_counters.txt",
-                               "src": "92e87f5640eb8a6c"},
-    ("sd3", "patch_attn"): {"mfma_busy": 0.355, "file": "profiles/attn_patch_sd3_mfma_counters.txt",
-                            "src": "92e87f5640eb8a6c"},
+    ("pixart", "patch_attn"): {"mfma_busy": 0.378, "file": "profiles/attn_patch_pixart_mfma_counters.txt",
+                               "src": "8ea515cefb0f3f25"},
+    ("sd3", "patch_attn"): {"mfma_busy": 0.353, "file": "profiles/attn_patch_sd3_mfma_counters.txt",
+                            "src": "8ea515cefb0f3f25"},
     ("flux", "chunk_attn"): {"mfma_busy": 0.531, "file": "profiles/attn_chunk_flux_mfma_counters.txt",
-                             "src": "92e87f5640eb8a6c"},
-    ("cog", "patch_attn"): {"mfma_busy": 0.409, "file": "profiles/attn_patch_cog_mfma_counters.txt",
-                            "src": "92e87f5640eb8a6c"},
-    ("cog", "chunk_attn"): {"mfma_busy": 0.453, "file": "profiles/attn_patch_cog_mfma_counters.txt",
-                            "src": "92e87f5640eb8a6c"},
+                             "src": "8ea515cefb0f3f25"},
+    ("cog", "patch_attn"): {"mfma_busy": 0.406, "file": "profiles/attn_patch_cog_mfma_counters.txt",
+                            "src": "8ea515cefb0f3f25"},
+    ("cog", "chunk_attn"): {"mfma_busy": 0.457, "file": "profiles/attn_patch_cog_mfma_counters.txt",
+                            "src": "8ea515cefb0f3f25"},
 }
 
 
