@@ -9,9 +9,10 @@ import numpy as np
 import pytest
 
 import oracle
+import paper_2411_01738_amd as xd
 from paper_2411_01738_amd.hotpath import HotPath
-from paper_2411_01738_amd.inputs import WORKLOADS, generate, sample_rows
-from tests.gpu_util import check_lse, check_out, to_np, torch_mod
+from paper_2411_01738_amd.inputs import WORKLOADS, generate, random_io, sample_rows
+from tests.gpu_util import check_lse, check_out, to_gpu, to_np, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -77,3 +78,25 @@ def test_sp_chunks_and_merge_full_size(name):
     ro, rl = orc.attention(q, t.k_fresh[:, c0:c1].copy(), t.v_fresh[:, c0:c1].copy(), rows=rows)
     check_out(to_np(hp.sp_out)[:, rows], ro, w.dtype, f"{name} merged")
     check_lse(to_np(hp.sp_lse)[:, :, rows], rl, w.dtype, f"{name} merged lse")
+
+
+@pytest.mark.parametrize("d", [64, 72])
+def test_large_grid_chunk_sampled(d):
+    """A chunk call with more 128-row query tiles than CUs (2 x 16 heads, 4096
+    queries over 8192 keys: 1024 tiles), the grid on which the library runs
+    its 4-wave workgroups two per CU at head dim <= 72; sampled rows against
+    the oracle, every tile edge of the first tiles among them."""
+    torch = torch_mod()
+    orc = oracle.get()
+    B, Nq, Nk, H = 2, 4096, 8192, 16
+    q = random_io((B, Nq, H, d), "bf16", 70 + d)
+    k = random_io((B, Nk, H, d), "bf16", 71 + d)
+    v = random_io((B, Nk, H, d), "bf16", 72 + d)
+    out = torch.full((B, Nq, H, d), float("nan"), device="cuda", dtype=torch.bfloat16)
+    lse = torch.full((B, H, Nq), float("nan"), device="cuda", dtype=torch.float32)
+    xd.xdit_chunk_attn(to_gpu(q, "bf16"), to_gpu(k, "bf16"), to_gpu(v, "bf16"), out, lse)
+    torch.cuda.synchronize()
+    rows = sample_rows(Nq, Nq // 24, [0, 31, 32, 63, 64, 127, 128, 255, 256, Nq - 1])
+    ro, rl = orc.attention(q, k, v, rows=rows)
+    check_out(to_np(out)[:, rows], ro, "bf16", f"large grid d={d}")
+    check_lse(to_np(lse)[:, :, rows], rl, "bf16", f"large grid lse d={d}")
